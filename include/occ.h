@@ -1,0 +1,234 @@
+/*
+ * occ.h -- resource-aware computation/communication overlap on one MI355X.
+ *
+ * C ABI of the hot path of "Resource-aware Computation-Communication Overlap
+ * for multi-GPU ML Workloads" (Cui, Pericas): a bf16 GEMM K_g whose
+ * per-workgroup LDS footprint shapes its occupancy (Section 3.1), run
+ * concurrently with one GPU's local share of a collective K_c (Background,
+ * item 2) on a second stream, with the per-iteration dependency
+ * K_g^i -> K_c^i enforced by an event (Section 3.2) and the collective given
+ * precedence over later GEMMs (Section 3.3).
+ *
+ * Conventions for every entry point:
+ *   - Device buffers are plain device pointers owned by the caller; the
+ *     library never allocates, frees or retains them.
+ *   - `stream` is a hipStream_t passed as void*; NULL means the null stream.
+ *     Kernel entry points are asynchronous: they return after enqueueing.
+ *   - Arguments are validated before any HIP call.  Errors are negative
+ *     occ_status codes; nothing is thrown across the ABI and nothing is
+ *     launched when a check fails.  occ_strerror() names each code.
+ *   - Not thread-safe: calls that overlap on one device from several host
+ *     threads must be serialised by the caller.
+ */
+#ifndef OCC_H
+#define OCC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum occ_status {
+  OCC_OK = 0,
+  OCC_EINVAL = -1,  /* null pointer, negative or unsupported size, misalignment */
+  OCC_ELDS = -2,    /* tile LDS + lds_bytes exceeds the per-workgroup LDS limit */
+  OCC_EPERM = -3,   /* perm is not a bijection of [0, nchunks) */
+  OCC_EALIAS = -4,  /* an output range overlaps an input range */
+  OCC_EHIP = -5,    /* the HIP runtime reported an error (launch, event, stream) */
+  OCC_ENODEV = -6   /* no gfx950 device is current */
+} occ_status;
+
+/* ------------------------------------------------------------------ K_g */
+
+/*
+ * occ_gemm -- C = A * op(B), bf16 inputs, fp32 accumulation, bf16 output.
+ * Background, item 1 (C = alpha op(A) op(B) + beta C) with alpha = 1,
+ * beta = 0 (C is overwritten, never read) and op(B) = B^T:
+ *   A : M x K, row-major bf16 (uint16 bit patterns), lda = K.
+ *   B : N x K, row-major bf16 -- the weight layout of a linear layer, so
+ *       C[m][n] = sum_k A[m][k] * B[n][k].
+ *   C : M x N, row-major bf16, ldc = N.  Rounded to nearest-even from fp32.
+ * lds_bytes is the EXTRA dynamic LDS each GEMM workgroup reserves on top of
+ * the LDS its tile uses (S_tile).  It is never touched; it only lowers the
+ * number of GEMM workgroups that fit on a CU (Section 3.1, S_blk).
+ * Requirements: M, N, K >= 0; K % 8 == 0; A, B, C 16-byte aligned;
+ * C must not overlap A or B.  M == 0 or N == 0 is a no-op; K == 0 writes
+ * zeros.  Returns OCC_ELDS if S_tile + lds_bytes exceeds the device's
+ * per-workgroup LDS limit (never clamps).
+ */
+int occ_gemm(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+             void *stream);
+
+/*
+ * Kernel variants (tile_m x tile_n x tile_k, waves, LDS stages).  Variant 0
+ * lets the library choose from the shape.  6 and 7 are the paper's tile
+ * configurations opt1 (64x64x32) and opt2 (64x64x64) of Table 1, with one LDS
+ * stage so that S_tile = 2*(TILE_M*TILE_K + TILE_K*TILE_N) bytes (Section 3.1).
+ */
+enum {
+  OCC_GEMM_AUTO = 0,
+  OCC_GEMM_256x256x64_4W = 1,
+  OCC_GEMM_256x256x64_8W = 2,
+  OCC_GEMM_256x128x64_4W = 3,
+  OCC_GEMM_256x128x64_4W_1STAGE = 4,
+  OCC_GEMM_128x128x64_4W = 5,
+  OCC_GEMM_OPT1_64x64x32 = 6,
+  OCC_GEMM_OPT2_64x64x64 = 7,
+  OCC_GEMM_SKINNY_M16 = 8,   /* M <= 16 only */
+  OCC_GEMM_256x256x32_4W_1STAGE = 9
+};
+
+/*
+ * occ_gemm_ex -- occ_gemm with an explicit kernel variant and grid cap.
+ * grid_cap > 0 launches at most grid_cap workgroups, each looping over output
+ * tiles (persistent workgroups): the "thread-block count" knob of the paper's
+ * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
+ * and the pad never change the result.  The tiled variants (all but 8)
+ * accumulate every output over k in the same order and give bit-identical
+ * results; the skinny variant splits K four ways and may differ from them in
+ * the last bit.  OCC_EINVAL for an unknown variant or the skinny variant
+ * with M > 16.
+ */
+int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                int variant, int grid_cap, void *stream);
+
+/* Launch plan occ_gemm_ex would use, for reporting and sweeps. */
+typedef struct occ_gemm_plan {
+  int tile_m, tile_n, tile_k;  /* output tile per workgroup and k-step */
+  int threads;                 /* threads per workgroup */
+  int tile_lds_bytes;          /* S_tile: LDS the tile itself uses */
+  int grid;                    /* workgroups launched */
+  int tiles;                   /* output tiles */
+  int wg_per_cu;               /* resident workgroups per CU with the pad (occupancy API) */
+  int max_lds_per_wg;          /* device limit on LDS per workgroup, bytes */
+  int lds_per_cu;              /* device LDS per CU, bytes */
+  int num_cus;                 /* compute units */
+  int kernel_id;               /* variant actually chosen */
+} occ_gemm_plan;
+
+/*
+ * occ_gemm_plan_query -- the plan for occ_gemm_ex(M, N, K, lds_bytes,
+ * variant, grid_cap) on the current device.  Returns OCC_ELDS when
+ * S_tile + lds_bytes exceeds the per-workgroup LDS limit (the plan is still
+ * filled in, with wg_per_cu = 0).
+ */
+int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
+                        occ_gemm_plan *plan);
+
+/* ------------------------------------------------------------------ K_c */
+
+/*
+ * share_reduce -- one GPU's local share of an allreduce (Background, item 2):
+ *   out[j] = (((bufs[0][j] + bufs[1][j]) + bufs[2][j]) + ...) + bufs[n-1][j]
+ * in IEEE binary32, strict left-to-right, for j < len.  Bit-identical to that
+ * definition (no reassociation, no contraction, denormals kept).
+ *   bufs    : HOST array of nchunks device pointers, 1 <= nchunks <= 64.
+ *   out     : device fp32 buffer of len elements; must not overlap any bufs[c].
+ * len == 0 is a no-op.  Any alignment is accepted; 16-byte-aligned buffers
+ * take the vectorised path.
+ */
+int share_reduce(const float *const *bufs, int nchunks, size_t len, float *out, void *stream);
+
+/*
+ * share_reduce_ex -- share_reduce with the comm-kernel knobs: `wgs`
+ * workgroups (0 = library default) and wave priority `priority` in 0..3
+ * (s_setprio; 0 = normal).  Same result for every wgs and priority.
+ */
+int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *out, int wgs,
+                    int priority, void *stream);
+
+/*
+ * share_permute -- one GPU's local share of an alltoall (Background, item 2):
+ * a chunk gather, dst[i*chunk_bytes + b] = src[perm[i]*chunk_bytes + b] for
+ * i < nchunks, b < chunk_bytes.  A byte copy: any dtype, bit-exact.
+ *   perm : HOST int32 array of nchunks entries, a bijection of [0, nchunks);
+ *          1 <= nchunks <= 512.
+ *   src, dst : device buffers of nchunks*chunk_bytes bytes; must not overlap.
+ * nchunks is an addition to the three-pointer form: the length of perm.
+ * chunk_bytes == 0 is a no-op.  16-byte-aligned src, dst and chunk_bytes take
+ * the vectorised path; anything else is copied byte by byte.
+ */
+int share_permute(const void *src, void *dst, const int32_t *perm, int nchunks, size_t chunk_bytes,
+                  void *stream);
+
+/* share_permute_ex -- share_permute with `wgs` and `priority` as share_reduce_ex. */
+int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunks,
+                     size_t chunk_bytes, int wgs, int priority, void *stream);
+
+/* ------------------------------------------------------------------ schedule */
+
+enum { OCC_COMM_REDUCE = 0, OCC_COMM_PERMUTE = 1 };
+
+/* run_overlap flags: which passes to time (default 0 means all three). */
+enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4 };
+
+typedef struct occ_overlap_cfg {
+  /* K_g: as occ_gemm */
+  int M, N, K;
+  const void *A, *B;
+  void *C;
+  size_t lds_bytes;         /* extra LDS per GEMM workgroup (Section 3.1) */
+  int gemm_variant;         /* OCC_GEMM_* (0 = automatic) */
+  int gemm_grid;            /* 0: one workgroup per tile; > 0: persistent grid cap */
+  /* K_c: as share_reduce (comm_kind 0) or share_permute (comm_kind 1) */
+  int comm_kind;
+  const float *const *bufs; /* host array of device pointers */
+  int nchunks;
+  size_t len;
+  float *out;
+  const void *src;
+  void *dst;
+  const int32_t *perm;      /* host array */
+  size_t chunk_bytes;
+  int comm_wgs;             /* workgroups of the comm kernel; 0 = library default */
+  int comm_priority;        /* wave priority of the comm kernel, 0 (normal) .. 3 (highest) */
+  /* schedule (Section 3.2) and protocol (Section 4.1) */
+  int n_iter;               /* GEMM -> collective iterations per schedule, >= 1 */
+  int reps;                 /* timed repetitions of each pass, >= 1 */
+  int warmup;               /* untimed repetitions before them, >= 0 */
+  int flags;                /* OCC_RUN_* bits, 0 = all */
+  /* optional device buffer of 4*n_iter uint64: for the last overlapped
+     repetition, [start_G0, end_G0, start_C0, end_C0, start_G1, ...] in
+     10 ns ticks of the GPU's constant-rate clock (earliest workgroup start,
+     latest workgroup end).  NULL = no timeline. */
+  uint64_t *timeline;
+} occ_overlap_cfg;
+
+typedef struct occ_overlap_result {
+  double t_seq_ms;        /* mean sequential makespan: one stream, G0 C0 G1 C1 ... */
+  double t_ovl_ms;        /* mean overlapped makespan: two streams + per-iteration event */
+  double t_seq_min_ms, t_ovl_min_ms;
+  double reduction_pct;   /* 100 * (1 - t_ovl / t_seq) = 100 * (1 - TimeRatio) */
+  double t_gemm_ms;       /* mean duration of one GEMM launch, isolated pass */
+  double t_comm_ms;       /* mean duration of one comm launch, isolated pass */
+  int gemm_wg_per_cu;     /* resident GEMM workgroups per CU (occupancy API) */
+  int gemm_grid;          /* GEMM workgroups per launch */
+  int gemm_tile_lds;      /* S_tile, bytes */
+  int comm_wgs;           /* comm workgroups per launch */
+} occ_overlap_result;
+
+/*
+ * run_overlap -- time the sequential and the overlapped schedule of n_iter
+ * GEMM -> collective iterations (Section 3.2, Fig. 1), after `warmup`
+ * untimed repetitions, averaging `reps` timed ones (Section 4.1).
+ * Host-synchronous.  Uses two library-owned streams of default priority on
+ * the current device (created once, kept for the process); the collective's
+ * precedence (Section 3.3) is the comm kernel's wave priority.  All three
+ * passes compute the same outputs: C, out/dst are identical to one occ_gemm
+ * and one share_* call.  Buffers are validated as by those entry points.
+ */
+int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
+
+/* Static string naming a status code. */
+const char *occ_strerror(int status);
+
+/* Library version, (major << 16) | minor. */
+int occ_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OCC_H */

@@ -1,0 +1,251 @@
+"""Python binding of libocc.so: the C entry points of include/occ.h, same names.
+
+Argument marshalling only: tensors become device pointers and sizes, the
+current torch stream becomes the hipStream_t, a non-zero status becomes an
+``OccError``.  Every step of the hot path runs in the library's HIP kernels;
+there is no fallback: if libocc.so is missing or no gfx950 GPU is current,
+the calls fail loudly.
+
+torch must be imported before the library is loaded so that both use the one
+HIP runtime already in the process (torch's; same soname).
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libocc.so")
+
+OCC_OK, OCC_EINVAL, OCC_ELDS, OCC_EPERM, OCC_EALIAS, OCC_EHIP, OCC_ENODEV = 0, -1, -2, -3, -4, -5, -6
+OCC_COMM_REDUCE, OCC_COMM_PERMUTE = 0, 1
+OCC_RUN_SEQ, OCC_RUN_OVL, OCC_RUN_ISO = 1, 2, 4
+GEMM_VARIANTS = {
+    0: "auto", 1: "256x256x64 4w", 2: "256x256x64 8w", 3: "256x128x64 4w",
+    4: "256x128x64 4w 1-stage", 5: "128x128x64 4w", 6: "opt1 64x64x32", 7: "opt2 64x64x64",
+    8: "skinny M<=16", 9: "256x256x32 4w 1-stage",
+}
+
+
+class OccError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s" % (where, occ_strerror(status)))
+
+
+class occ_gemm_plan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "tile_m", "tile_n", "tile_k", "threads", "tile_lds_bytes", "grid", "tiles", "wg_per_cu",
+        "max_lds_per_wg", "lds_per_cu", "num_cus", "kernel_id")]
+
+
+class occ_overlap_cfg(ctypes.Structure):
+    _fields_ = [
+        ("M", ctypes.c_int), ("N", ctypes.c_int), ("K", ctypes.c_int),
+        ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
+        ("lds_bytes", ctypes.c_size_t), ("gemm_variant", ctypes.c_int), ("gemm_grid", ctypes.c_int),
+        ("comm_kind", ctypes.c_int), ("bufs", ctypes.POINTER(ctypes.c_void_p)),
+        ("nchunks", ctypes.c_int), ("len", ctypes.c_size_t), ("out", ctypes.c_void_p),
+        ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("perm", ctypes.POINTER(ctypes.c_int32)),
+        ("chunk_bytes", ctypes.c_size_t), ("comm_wgs", ctypes.c_int), ("comm_priority", ctypes.c_int),
+        ("n_iter", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
+        ("flags", ctypes.c_int), ("timeline", ctypes.c_void_p),
+    ]
+
+
+class occ_overlap_result(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in (
+        "t_seq_ms", "t_ovl_ms", "t_seq_min_ms", "t_ovl_min_ms", "reduction_pct", "t_gemm_ms",
+        "t_comm_ms")] + [(n, ctypes.c_int) for n in (
+            "gemm_wg_per_cu", "gemm_grid", "gemm_tile_lds", "comm_wgs")]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_SIGS = {
+    "occ_gemm": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
+    "occ_gemm_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
+                    ctypes.c_int, ctypes.c_int, _P],
+    "occ_gemm_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
+                            ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
+    "share_reduce": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, _P],
+    "share_reduce_ex": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, ctypes.c_int,
+                        ctypes.c_int, _P],
+    "share_permute": [_P, _P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t, _P],
+    "share_permute_ex": [_P, _P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t,
+                         ctypes.c_int, ctypes.c_int, _P],
+    "run_overlap": [ctypes.POINTER(occ_overlap_cfg), ctypes.POINTER(occ_overlap_result)],
+    "occ_strerror": [ctypes.c_int],
+    "occ_version": [],
+}
+
+
+def lib():
+    """The loaded libocc.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libocc.so is not built (%s); run python -m paper_2606_09200_amd.build"
+                               % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        for name, args in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = ctypes.c_char_p if name == "occ_strerror" else ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def occ_strerror(status):
+    return lib().occ_strerror(int(status)).decode()
+
+
+def occ_version():
+    v = lib().occ_version()
+    return (v >> 16, v & 0xFFFF)
+
+
+def _check(status, where):
+    if status != OCC_OK:
+        raise OccError(status, where)
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
+
+
+def _gemm_args(A, B, C):
+    for name, t in (("A", A), ("B", B), ("C", C)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 2:
+            raise ValueError("%s must be a contiguous 2-D bfloat16 GPU tensor" % name)
+    M, K = A.shape
+    N = B.shape[0]
+    if B.shape[1] != K or tuple(C.shape) != (M, N):
+        raise ValueError("shapes must be A (M,K), B (N,K), C (M,N)")
+    return M, N, K
+
+
+def occ_gemm(A, B, C, lds_bytes=0, stream=None):
+    """C = A @ B.T (bf16, fp32 accumulation); B is N x K."""
+    M, N, K = _gemm_args(A, B, C)
+    _check(lib().occ_gemm(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), _stream(stream)),
+           "occ_gemm")
+    return C
+
+
+def occ_gemm_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
+    M, N, K = _gemm_args(A, B, C)
+    _check(lib().occ_gemm_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
+                             int(grid_cap), _stream(stream)), "occ_gemm_ex")
+    return C
+
+
+def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False):
+    """Plan as a dict; 'feasible' is False when the pad does not fit (OCC_ELDS)."""
+    p = occ_gemm_plan()
+    st = lib().occ_gemm_plan_query(int(M), int(N), int(K), int(lds_bytes), int(variant),
+                                   int(grid_cap), ctypes.byref(p))
+    if st not in (OCC_OK, OCC_ELDS) or (strict and st != OCC_OK):
+        raise OccError(st, "occ_gemm_plan_query")
+    d = {f: getattr(p, f) for f, _ in occ_gemm_plan._fields_}
+    d["feasible"] = st == OCC_OK
+    return d
+
+
+def _chunk_ptrs(bufs):
+    if isinstance(bufs, torch.Tensor):
+        bufs = list(bufs.unbind(0)) if bufs.dim() == 2 else [bufs]
+    for b in bufs:
+        if b.dtype != torch.float32 or not b.is_cuda or not b.is_contiguous():
+            raise ValueError("chunks must be contiguous float32 GPU tensors")
+    length = bufs[0].numel() if bufs else 0
+    if any(b.numel() != length for b in bufs):
+        raise ValueError("all chunks must have the same length")
+    arr = (ctypes.c_void_p * max(1, len(bufs)))(*[b.data_ptr() for b in bufs])
+    return arr, len(bufs), length
+
+
+def share_reduce(bufs, out, stream=None, wgs=0, priority=0):
+    """out = bufs[0] + bufs[1] + ... (binary32, left to right)."""
+    arr, n, length = _chunk_ptrs(bufs)
+    if out.dtype != torch.float32 or not out.is_cuda or out.numel() != length:
+        raise ValueError("out must be a float32 GPU tensor of the chunk length")
+    if wgs or priority:
+        st = lib().share_reduce_ex(arr, n, length, _ptr(out), int(wgs), int(priority), _stream(stream))
+    else:
+        st = lib().share_reduce(arr, n, length, _ptr(out), _stream(stream))
+    _check(st, "share_reduce")
+    return out
+
+
+def _perm_arr(perm):
+    p = [int(x) for x in (perm.tolist() if hasattr(perm, "tolist") else perm)]
+    return (ctypes.c_int32 * max(1, len(p)))(*p), len(p)
+
+
+def share_permute(src, dst, perm, chunk_bytes, stream=None, wgs=0, priority=0):
+    """dst chunk i = src chunk perm[i] (byte copy)."""
+    arr, n = _perm_arr(perm)
+    for name, t in (("src", src), ("dst", dst)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous GPU tensor" % name)
+        if t.numel() * t.element_size() != n * chunk_bytes:
+            raise ValueError("%s must hold nchunks * chunk_bytes bytes" % name)
+    if wgs or priority:
+        st = lib().share_permute_ex(_ptr(src), _ptr(dst), arr, n, int(chunk_bytes), int(wgs),
+                                    int(priority), _stream(stream))
+    else:
+        st = lib().share_permute(_ptr(src), _ptr(dst), arr, n, int(chunk_bytes), _stream(stream))
+    _check(st, "share_permute")
+    return dst
+
+
+def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
+                lds_bytes=0, gemm_variant=0, gemm_grid=0, comm_wgs=0, comm_priority=3, n_iter=10,
+                reps=20, warmup=10, flags=0, timeline=None):
+    """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
+
+    Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
+    ``chunk_bytes`` for the alltoall share.  ``timeline``: optional uint64 GPU
+    tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).
+    Returns the occ_overlap_result fields as a dict.
+    """
+    M, N, K = _gemm_args(A, B, C)
+    cfg = occ_overlap_cfg()
+    cfg.M, cfg.N, cfg.K = M, N, K
+    cfg.A, cfg.B, cfg.C = _ptr(A).value, _ptr(B).value, _ptr(C).value
+    cfg.lds_bytes, cfg.gemm_variant, cfg.gemm_grid = int(lds_bytes), int(gemm_variant), int(gemm_grid)
+    keep = []
+    if bufs is not None:
+        arr, n, length = _chunk_ptrs(bufs)
+        keep.append(arr)
+        cfg.comm_kind = OCC_COMM_REDUCE
+        cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+        cfg.nchunks, cfg.len, cfg.out = n, length, _ptr(out).value
+        if out.numel() != length or out.dtype != torch.float32:
+            raise ValueError("out must be float32 of the chunk length")
+    else:
+        parr, n = _perm_arr(perm)
+        keep.append(parr)
+        cfg.comm_kind = OCC_COMM_PERMUTE
+        cfg.src, cfg.dst = _ptr(src).value, _ptr(dst).value
+        cfg.perm = ctypes.cast(parr, ctypes.POINTER(ctypes.c_int32))
+        cfg.nchunks, cfg.chunk_bytes = n, int(chunk_bytes)
+        for t in (src, dst):
+            if t.numel() * t.element_size() != n * chunk_bytes:
+                raise ValueError("src/dst must hold nchunks * chunk_bytes bytes")
+    cfg.comm_wgs, cfg.comm_priority = int(comm_wgs), int(comm_priority)
+    cfg.n_iter, cfg.reps, cfg.warmup, cfg.flags = int(n_iter), int(reps), int(warmup), int(flags)
+    if timeline is not None:
+        if timeline.dtype not in (torch.int64, torch.uint64) or timeline.numel() < 4 * n_iter:
+            raise ValueError("timeline must hold 4*n_iter 64-bit entries")
+        cfg.timeline = timeline.data_ptr()
+    res = occ_overlap_result()
+    _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
+    return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}

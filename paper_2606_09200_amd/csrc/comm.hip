@@ -1,0 +1,259 @@
+// K_c: one GPU's local share of a collective (Background, item 2).
+//
+//   share_reduce  -- allreduce share: fixed-order binary32 sum of the chunks.
+//   share_permute -- alltoall share: gather of whole chunks by a permutation.
+//
+// Both are HBM-bound streams: 16-byte non-temporal loads and stores (so the
+// stream does not evict the concurrently running GEMM's operands from L2),
+// several independent loads in flight per lane, and a grid that is a knob
+// (communication kernels are meant to be light, Section 3.1).  The comm
+// kernel's wave priority is raised with s_setprio when asked: that is how the
+// collective is given precedence over co-resident GEMM waves (Section 3.3).
+#include "device_util.h"
+#include "occ_internal.h"
+
+#include <string.h>
+
+namespace occ {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+
+struct ChunkPtrs {
+  const float *p[kMaxReduceChunks];
+};
+
+// Vector path: all chunk pointers and out are 16-byte aligned.  Element j's
+// sum is acc = c0[j]; acc = acc + c1[j]; ... exactly in chunk order; the
+// loads of all chunks for UNROLL positions are issued before any addition.
+template <int NC, int UNROLL>
+__global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
+                                                              float *__restrict__ out, int prio,
+                                                              uint64_t *stamps) {
+  set_wave_priority(prio);
+  stamp_begin(stamps);
+  const int nc = NC > 0 ? NC : nchunks;
+  const size_t stride = (size_t)gridDim.x * kThreads;
+  size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  f32x4 *o = reinterpret_cast<f32x4 *>(out);
+
+  if constexpr (NC > 0) {
+    for (; i + (UNROLL - 1) * stride < nvec; i += UNROLL * stride) {
+      f32x4 v[NC][UNROLL];
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+          v[c][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[c]) + i + u * stride);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        f32x4 acc = v[0][u];
+#pragma unroll
+        for (int c = 1; c < NC; ++c) {
+          acc[0] = acc[0] + v[c][u][0];
+          acc[1] = acc[1] + v[c][u][1];
+          acc[2] = acc[2] + v[c][u][2];
+          acc[3] = acc[3] + v[c][u][3];
+        }
+        __builtin_nontemporal_store(acc, o + i + u * stride);
+      }
+    }
+  }
+  // Remaining positions (and every position when the chunk count is only
+  // known at run time): chunks in batches of 8 loads, folded in order.
+  for (; i < nvec; i += stride) {
+    f32x4 acc = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[0]) + i);
+    for (int c0 = 1; c0 < nc; c0 += 8) {
+      f32x4 v[8];
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        if (c0 + c < nc) v[c] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[c0 + c]) + i);
+#pragma unroll
+      for (int c = 0; c < 8; ++c)
+        if (c0 + c < nc) {
+          acc[0] = acc[0] + v[c][0];
+          acc[1] = acc[1] + v[c][1];
+          acc[2] = acc[2] + v[c][2];
+          acc[3] = acc[3] + v[c][3];
+        }
+    }
+    __builtin_nontemporal_store(acc, o + i);
+  }
+  stamp_end(stamps);
+}
+
+// Scalar path: elements [first, len) one at a time (the tail after the vector
+// path, or everything when a buffer is not 16-byte aligned).
+__global__ __launch_bounds__(kThreads) void reduce_scalar_kernel(ChunkPtrs cp, int nchunks,
+                                                                 size_t first, size_t len,
+                                                                 float *__restrict__ out, int prio,
+                                                                 uint64_t *stamps) {
+  set_wave_priority(prio);
+  stamp_begin(stamps);
+  const size_t stride = (size_t)gridDim.x * kThreads;
+  for (size_t j = first + (size_t)blockIdx.x * kThreads + threadIdx.x; j < len; j += stride) {
+    float acc = cp.p[0][j];
+    for (int c = 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
+    out[j] = acc;
+  }
+  stamp_end(stamps);
+}
+
+struct PermTable {
+  int32_t p[kMaxPermuteChunks];
+};
+
+// Permutation copy, 16-byte units.  Work item w covers part (w % parts) of
+// destination chunk (w / parts); workgroups stride over work items, threads
+// over the part's units with UNROLL loads in flight before the stores.
+template <int UNROLL>
+__global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
+                                                               u32x4 *__restrict__ dst, PermTable pt,
+                                                               int nchunks, size_t cvec, int parts,
+                                                               int prio, uint64_t *stamps) {
+  set_wave_priority(prio);
+  stamp_begin(stamps);
+  const int nwork = nchunks * parts;
+  for (int w = blockIdx.x; w < nwork; w += gridDim.x) {
+    const int chunk = w / parts;
+    const int part = w - chunk * parts;
+    const size_t lo = cvec * part / parts;
+    const size_t hi = cvec * (part + 1) / parts;
+    const u32x4 *s = src + (size_t)pt.p[chunk] * cvec;
+    u32x4 *d = dst + (size_t)chunk * cvec;
+    size_t i = lo + threadIdx.x;
+    for (; i + (UNROLL - 1) * kThreads < hi; i += UNROLL * kThreads) {
+      u32x4 v[UNROLL];
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(s + i + u * kThreads);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) __builtin_nontemporal_store(v[u], d + i + u * kThreads);
+    }
+    for (; i < hi; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+  }
+  stamp_end(stamps);
+}
+
+// Byte path for unaligned buffers or chunk sizes.
+__global__ __launch_bounds__(kThreads) void permute_byte_kernel(const uint8_t *__restrict__ src,
+                                                                uint8_t *__restrict__ dst,
+                                                                PermTable pt, int nchunks,
+                                                                size_t chunk_bytes, int prio,
+                                                                uint64_t *stamps) {
+  set_wave_priority(prio);
+  stamp_begin(stamps);
+  const size_t stride = (size_t)gridDim.x * kThreads;
+  for (int c = 0; c < nchunks; ++c) {
+    const uint8_t *s = src + (size_t)pt.p[c] * chunk_bytes;
+    uint8_t *d = dst + (size_t)c * chunk_bytes;
+    for (size_t b = (size_t)blockIdx.x * kThreads + threadIdx.x; b < chunk_bytes; b += stride) d[b] = s[b];
+  }
+  stamp_end(stamps);
+}
+
+__global__ void stamps_reset_kernel(uint64_t *stamps, int npairs) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < npairs) {
+    stamps[2 * i] = ~0ull;
+    stamps[2 * i + 1] = 0ull;
+  }
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int clamp_wgs(size_t work_units, int wanted) {
+  size_t cap = (work_units + kThreads - 1) / kThreads;
+  if (cap < 1) cap = 1;
+  return (int)(wanted < (long long)cap ? wanted : cap);
+}
+
+}  // namespace
+
+int reduce_default_wgs(const ReduceCall &c) {
+  const DeviceInfo *di = nullptr;
+  int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
+  return clamp_wgs(c.len / 4 + 1, 2 * cus);
+}
+
+int reduce_launch(const ReduceCall &c, hipStream_t s) {
+  if (c.len == 0) return OCC_OK;
+  ChunkPtrs cp;
+  memset(&cp, 0, sizeof cp);
+  bool vec = aligned16(c.out);
+  for (int i = 0; i < c.nchunks; ++i) {
+    cp.p[i] = c.bufs[i];
+    vec = vec && aligned16(c.bufs[i]);
+  }
+  int wgs = c.wgs > 0 ? c.wgs : reduce_default_wgs(c);
+  const int prio = c.priority;
+  if (vec) {
+    size_t nvec = c.len / 4;
+    if (nvec > 0) {
+      int g = clamp_wgs(nvec, wgs);
+      switch (c.nchunks) {
+        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+      }
+    }
+    size_t first = nvec * 4;
+    if (first < c.len)
+      hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kThreads), 0, s, cp, c.nchunks, first,
+                         c.len, c.out, prio, c.stamps);
+  } else {
+    hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs)), dim3(kThreads), 0, s, cp,
+                       c.nchunks, (size_t)0, c.len, c.out, prio, c.stamps);
+  }
+  return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
+}
+
+static int permute_parts(size_t chunk_bytes) {
+  // about 256 KiB per work item, at least one
+  size_t parts = (chunk_bytes + (256u << 10) - 1) / (256u << 10);
+  if (parts < 1) parts = 1;
+  if (parts > 4096) parts = 4096;
+  return (int)parts;
+}
+
+int permute_default_wgs(const PermuteCall &c) {
+  const DeviceInfo *di = nullptr;
+  int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
+  long long items = (long long)c.nchunks * permute_parts(c.chunk_bytes);
+  long long want = 2LL * cus;
+  return (int)(items < want ? items : want);
+}
+
+int permute_launch(const PermuteCall &c, hipStream_t s) {
+  if (c.chunk_bytes == 0) return OCC_OK;
+  PermTable pt;
+  memset(&pt, 0, sizeof pt);
+  for (int i = 0; i < c.nchunks; ++i) pt.p[i] = c.perm[i];
+  int wgs = c.wgs > 0 ? c.wgs : permute_default_wgs(c);
+  if (aligned16(c.src) && aligned16(c.dst) && c.chunk_bytes % 16 == 0) {
+    int parts = permute_parts(c.chunk_bytes);
+    long long items = (long long)c.nchunks * parts;
+    int g = (int)(wgs < items ? wgs : items);
+    hipLaunchKernelGGL((permute_vec_kernel<4>), dim3(g), dim3(kThreads), 0, s,
+                       static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
+                       c.chunk_bytes / 16, parts, c.priority, c.stamps);
+  } else {
+    int g = clamp_wgs(c.chunk_bytes, wgs);
+    hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kThreads), 0, s,
+                       static_cast<const uint8_t *>(c.src), static_cast<uint8_t *>(c.dst), pt,
+                       c.nchunks, c.chunk_bytes, c.priority, c.stamps);
+  }
+  return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
+}
+
+int stamps_reset(uint64_t *stamps, int npairs, hipStream_t s) {
+  if (stamps == nullptr || npairs <= 0) return OCC_OK;
+  hipLaunchKernelGGL(stamps_reset_kernel, dim3((npairs + 255) / 256), dim3(256), 0, s, stamps, npairs);
+  return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
+}
+
+}  // namespace occ

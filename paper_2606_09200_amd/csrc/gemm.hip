@@ -1,0 +1,454 @@
+// K_g: bf16 GEMM C = A * B^T on MFMA (gfx950), fp32 accumulation, bf16 output.
+//
+// Background, item 1: the GEMM of a linear layer, tiled and staged through
+// on-chip memory.  Section 3.1: the LDS a workgroup allocates,
+// S_blk ~ TILE_M*TILE_K + TILE_K*TILE_N, bounds how many GEMM workgroups
+// reside on a CU; an extra dynamic-LDS pad on top of the tile's own LDS lowers
+// that residency without changing the kernel's arithmetic.
+//
+// Layout: A is M x K, B is N x K (both K-contiguous, so both MFMA operands are
+// read from LDS as 16-byte rows), C is M x N, all row-major.
+#include "device_util.h"
+#include "occ_internal.h"
+
+#include <algorithm>
+
+namespace occ {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));  // round to nearest even
+}
+
+// ---------------------------------------------------------------------------
+// Tiled kernel.  A workgroup owns a BM x BN output tile; WM x WN waves each
+// own a (BM/WM) x (BN/WN) sub-tile made of 32x32 MFMA blocks.  Each k-step of
+// BK is staged into LDS ([rows][BK] bf16, 16-byte chunks XOR-swizzled by row
+// so that the 32 rows of an MFMA operand read hit distinct banks), with the
+// next k-step's global loads in flight in registers while the current one is
+// multiplied.  STAGES = 2 double-buffers the LDS (one barrier per k-step).
+template <int BM_, int BN_, int BK_, int WM_, int WN_, int STAGES_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int NT = 64 * WM * WN;
+  static constexpr int TM = BM / WM, TN = BN / WN;
+  static constexpr int FM = TM / 32, FN = TN / 32;
+  static constexpr int KCH = BK / 8;              // 16-byte chunks per tile row
+  static constexpr int ROWS_PER_PASS = NT / KCH;  // rows the workgroup loads per pass
+  static constexpr int A_LOADS = BM / ROWS_PER_PASS;
+  static constexpr int B_LOADS = BN / ROWS_PER_PASS;
+  static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be whole 32x32 blocks");
+  static_assert(KCH == 4 || KCH == 8, "BK must be 32 or 64");
+  static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small for the workgroup");
+  static_assert(BM % ROWS_PER_PASS == 0 && BN % ROWS_PER_PASS == 0, "uneven load passes");
+};
+
+// Physical 16-byte chunk of logical chunk c in tile row r.
+template <int KCH>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (KCH == 8) return c ^ (r & 7);
+  else return c ^ ((r >> 1) & 3);
+}
+
+// XCD-aware order: dispatch hands consecutive workgroups to the 8 XCDs in
+// turn, so tile ids are regrouped to give each XCD a contiguous run of the
+// grouped order below (and thus shared A/B panels in its own L2).
+__device__ __forceinline__ int xcd_remap(int t, int n) {
+  int full = n & ~7;
+  if (t >= full) return t;
+  return (t & 7) * (full >> 3) + (t >> 3);
+}
+
+// Grouped tile order: GROUP tile-rows at a time, column-major inside a group.
+template <int GROUP>
+__device__ __forceinline__ void tile_coords(int id, int tiles_m, int tiles_n, int &tm, int &tn) {
+  int per_group = GROUP * tiles_n;
+  int g = id / per_group;
+  int first = g * GROUP;
+  int gs = min(tiles_m - first, GROUP);
+  int in = id - g * per_group;
+  tm = first + in % gs;
+  tn = in / gs;
+}
+
+template <class T>
+__device__ __forceinline__ void load_tile_regs(const uint16_t *__restrict__ A,
+                                               const uint16_t *__restrict__ B, int M, int N,
+                                               int K, int m0, int n0, int k0, u32x4 (&ra)[T::A_LOADS],
+                                               u32x4 (&rb)[T::B_LOADS]) {
+  const int tid = threadIdx.x;
+  const int r_in = tid / T::KCH;
+  const int c = tid % T::KCH;
+  const int k = k0 + c * 8;
+  const bool kok = k < K;
+#pragma unroll
+  for (int p = 0; p < T::A_LOADS; ++p) {
+    int m = m0 + p * T::ROWS_PER_PASS + r_in;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (kok && m < M) v = *reinterpret_cast<const u32x4 *>(A + (size_t)m * K + k);
+    ra[p] = v;
+  }
+#pragma unroll
+  for (int p = 0; p < T::B_LOADS; ++p) {
+    int n = n0 + p * T::ROWS_PER_PASS + r_in;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (kok && n < N) v = *reinterpret_cast<const u32x4 *>(B + (size_t)n * K + k);
+    rb[p] = v;
+  }
+}
+
+template <class T>
+__device__ __forceinline__ void store_tile_lds(unsigned char *stage, const u32x4 (&ra)[T::A_LOADS],
+                                               const u32x4 (&rb)[T::B_LOADS]) {
+  const int tid = threadIdx.x;
+  const int r_in = tid / T::KCH;
+  const int c = tid % T::KCH;
+#pragma unroll
+  for (int p = 0; p < T::A_LOADS; ++p) {
+    int r = p * T::ROWS_PER_PASS + r_in;
+    *reinterpret_cast<u32x4 *>(stage + r * (T::BK * 2) + swz<T::KCH>(r, c) * 16) = ra[p];
+  }
+  unsigned char *bs = stage + T::A_BYTES;
+#pragma unroll
+  for (int p = 0; p < T::B_LOADS; ++p) {
+    int r = p * T::ROWS_PER_PASS + r_in;
+    *reinterpret_cast<u32x4 *>(bs + r * (T::BK * 2) + swz<T::KCH>(r, c) * 16) = rb[p];
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__restrict__ A,
+                                                           const uint16_t *__restrict__ B,
+                                                           uint16_t *__restrict__ C, int M, int N,
+                                                           int K, int tiles_m, int tiles_n,
+                                                           uint64_t *stamps) {
+  extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
+  stamp_begin(stamps);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / T::WN;
+  const int wn = wave % T::WN;
+  const int ntiles = tiles_m * tiles_n;
+  const int nk = (K + T::BK - 1) / T::BK;
+
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int tm, tn;
+    tile_coords<8>(xcd_remap(t, ntiles), tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * T::BM;
+    const int n0 = tn * T::BN;
+
+    f32x16 acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    u32x4 ra[T::A_LOADS], rb[T::B_LOADS];
+    if (nk > 0) {
+      load_tile_regs<T>(A, B, M, N, K, m0, n0, 0, ra, rb);
+      store_tile_lds<T>(smem, ra, rb);
+    }
+    __syncthreads();
+
+    // Per-lane LDS offsets of the MFMA operand rows for each 16-wide k-substep.
+    const int arow = wm * T::TM + (lane & 31);
+    const int brow = wn * T::TN + (lane & 31);
+    const int half = lane >> 5;
+
+    for (int kt = 0; kt < nk; ++kt) {
+      unsigned char *cur = smem + (kt % T::STAGES) * T::STAGE_BYTES;
+      const bool more = kt + 1 < nk;
+      if (more) load_tile_regs<T>(A, B, M, N, K, m0, n0, (kt + 1) * T::BK, ra, rb);
+
+#pragma unroll
+      for (int ks = 0; ks < T::BK / 16; ++ks) {
+        const int c = ks * 2 + half;
+        bf16x8 af[T::FM], bfr[T::FN];
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i) {
+          int r = arow + i * 32;
+          af[i] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4 *>(cur + r * (T::BK * 2) + swz<T::KCH>(r, c) * 16));
+        }
+        const unsigned char *bs = cur + T::A_BYTES;
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) {
+          int r = brow + j * 32;
+          bfr[j] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * (T::BK * 2) + swz<T::KCH>(r, c) * 16));
+        }
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < T::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+
+      if constexpr (T::STAGES == 1) __syncthreads();
+      if (more) store_tile_lds<T>(smem + ((kt + 1) % T::STAGES) * T::STAGE_BYTES, ra, rb);
+      __syncthreads();
+    }
+
+    // Epilogue.  32x32 MFMA result layout: lane holds column (lane % 32) and
+    // rows 8*(r/4) + 4*(lane/32) + r%4 of the block, r = 0..15.
+    const int ncol = lane & 31;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j) {
+        const int n = n0 + wn * T::TN + j * 32 + ncol;
+        const int mb = m0 + wm * T::TM + i * 32 + 4 * half;
+        if (n < N) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = mb + 8 * (r >> 2) + (r & 3);
+            if (m < M) C[(size_t)m * N + n] = to_bf16(acc[i][j][r]);
+          }
+        }
+      }
+    }
+  }
+  stamp_end(stamps);
+}
+
+// ---------------------------------------------------------------------------
+// Skinny kernel for M <= 16 (decode-like GEMMs, HBM-bound on B).  A workgroup
+// owns 16 output columns; its 4 waves split K into contiguous quarters and
+// each streams its share of 16 rows of B straight from HBM into 16x16x32
+// MFMA operands (no LDS staging: every B element is used exactly once).
+// The four partial 16x16 sums are added in wave order 0+1+2+3 through LDS,
+// so the result does not depend on timing.
+constexpr int kSkinnyKB = 128;  // k covered by one wave per block (4 MFMAs)
+
+__global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__restrict__ A,
+                                                          const uint16_t *__restrict__ B,
+                                                          uint16_t *__restrict__ C, int M, int N,
+                                                          int K, uint64_t *stamps) {
+  __shared__ f32x4 partial[3][64];
+  extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
+  (void)pad_lds;
+  stamp_begin(stamps);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r = lane & 15;   // A row / B row (output column) this lane feeds
+  const int g = lane >> 4;   // k group
+  const int n0 = blockIdx.x * 16;
+  const int nblk = (K + kSkinnyKB - 1) / kSkinnyKB;
+  const int b0 = wave * nblk / 4, b1 = (wave + 1) * nblk / 4;
+  const bool arow_ok = r < M;
+  const bool brow_ok = n0 + r < N;
+  const uint16_t *arow = A + (size_t)(arow_ok ? r : 0) * K;
+  const uint16_t *brow = B + (size_t)(brow_ok ? n0 + r : 0) * K;
+
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  int b = b0;
+  for (; b + 1 < b1; b += 2) {
+    u32x4 av[8], bv[8];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        int k = (b + u) * kSkinnyKB + g * 32 + s * 8;
+        u32x4 za = {0u, 0u, 0u, 0u}, zb = {0u, 0u, 0u, 0u};
+        if (k < K) {
+          if (arow_ok) za = *reinterpret_cast<const u32x4 *>(arow + k);
+          if (brow_ok) zb = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(brow + k));
+        }
+        av[u * 4 + s] = za;
+        bv[u * 4 + s] = zb;
+      }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[q]),
+                                                    __builtin_bit_cast(bf16x8, bv[q]), acc, 0, 0, 0);
+  }
+  for (; b < b1; ++b) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      int k = b * kSkinnyKB + g * 32 + s * 8;
+      u32x4 za = {0u, 0u, 0u, 0u}, zb = {0u, 0u, 0u, 0u};
+      if (k < K) {
+        if (arow_ok) za = *reinterpret_cast<const u32x4 *>(arow + k);
+        if (brow_ok) zb = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(brow + k));
+      }
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, za),
+                                                    __builtin_bit_cast(bf16x8, zb), acc, 0, 0, 0);
+    }
+  }
+
+  if (wave > 0) partial[wave - 1][lane] = acc;
+  __syncthreads();
+  if (wave == 0) {
+    f32x4 s = acc;
+#pragma unroll
+    for (int w = 0; w < 3; ++w) {
+      f32x4 p = partial[w][lane];
+      s[0] = s[0] + p[0];
+      s[1] = s[1] + p[1];
+      s[2] = s[2] + p[2];
+      s[3] = s[3] + p[3];
+    }
+    // 16x16 MFMA result layout: lane holds column (lane % 16), rows 4*(lane/16) + i.
+    const int n = n0 + r;
+    if (n < N) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int m = 4 * g + i;
+        if (m < M) C[(size_t)m * N + n] = to_bf16(s[i]);
+      }
+    }
+  }
+  stamp_end(stamps);
+}
+
+// ---------------------------------------------------------------------------
+// Variant table.
+typedef void (*TiledFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, int,
+                        uint64_t *);
+
+struct Variant {
+  int id;
+  int bm, bn, bk, threads, lds;
+  TiledFn fn;  // null: the skinny kernel
+  const char *name;
+};
+
+template <class T>
+constexpr Variant make_variant(int id, const char *name) {
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, name};
+}
+
+using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
+using T256x256_8w = Tile<256, 256, 64, 2, 4, 2>;
+using T256x128_4w = Tile<256, 128, 64, 2, 2, 2>;
+using T256x128_4w_1s = Tile<256, 128, 64, 2, 2, 1>;
+using T128x128_4w = Tile<128, 128, 64, 2, 2, 2>;
+using T64x64_opt1 = Tile<64, 64, 32, 2, 2, 1>;   // Table 1 opt1: 64x64x32
+using T64x64_opt2 = Tile<64, 64, 64, 2, 2, 1>;   // Table 1 opt2: 64x64x64
+using T256x256_k32_1s = Tile<256, 256, 32, 2, 2, 1>;
+
+constexpr int kSkinnyId = 8;
+constexpr int kSkinnyStaticLds = 3 * 64 * 16;
+
+const Variant kVariants[] = {
+    make_variant<T256x256_4w>(1, "256x256x64 4w 2st"),
+    make_variant<T256x256_8w>(2, "256x256x64 8w 2st"),
+    make_variant<T256x128_4w>(3, "256x128x64 4w 2st"),
+    make_variant<T256x128_4w_1s>(4, "256x128x64 4w 1st"),
+    make_variant<T128x128_4w>(5, "128x128x64 4w 2st"),
+    make_variant<T64x64_opt1>(6, "64x64x32 opt1"),
+    make_variant<T64x64_opt2>(7, "64x64x64 opt2"),
+    Variant{kSkinnyId, 16, 16, kSkinnyKB, 256, kSkinnyStaticLds, nullptr, "skinny M<=16"},
+    make_variant<T256x256_k32_1s>(9, "256x256x32 4w 1st"),
+};
+
+const Variant *find_variant(int id) {
+  for (const Variant &v : kVariants)
+    if (v.id == id) return &v;
+  return nullptr;
+}
+
+int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+int auto_variant(int M, int N, int K, int num_cus) {
+  (void)K;
+  if (M <= 16) return kSkinnyId;
+  long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
+  if (big >= num_cus) return 1;
+  long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
+  if (mid >= num_cus / 2) return 5;
+  return 7;
+}
+
+}  // namespace
+
+static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_gemm_plan *p) {
+  const Variant *v = find_variant(variant);
+  if (v == nullptr) return OCC_EINVAL;
+  if (variant == kSkinnyId && c.M > 16) return OCC_EINVAL;
+  p->tile_m = v->bm;
+  p->tile_n = v->bn;
+  p->tile_k = v->bk;
+  p->threads = v->threads;
+  p->tile_lds_bytes = v->lds;
+  p->tiles = variant == kSkinnyId ? ceil_div(c.N, 16) : ceil_div(c.M, v->bm) * ceil_div(c.N, v->bn);
+  p->grid = p->tiles;
+  if (variant != kSkinnyId && c.grid_cap > 0 && c.grid_cap < p->grid) p->grid = c.grid_cap;
+  p->max_lds_per_wg = di.max_lds_per_wg;
+  p->lds_per_cu = di.lds_per_cu;
+  p->num_cus = di.num_cus;
+  p->kernel_id = variant;
+  p->wg_per_cu = 0;
+  if (c.lds_bytes > (size_t)di.max_lds_per_wg ||
+      (size_t)v->lds + c.lds_bytes > (size_t)di.max_lds_per_wg)
+    return OCC_ELDS;
+  return OCC_OK;
+}
+
+int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
+  const DeviceInfo *di = nullptr;
+  int st = current_device_info(&di);
+  if (st != OCC_OK) return st;
+  int variant = c.variant;
+  if (variant == 0) variant = auto_variant(c.M, c.N, c.K, di->num_cus);
+  st = fill_plan(c, variant, *di, plan);
+  if (st != OCC_OK) return st;
+  const Variant *v = find_variant(variant);
+  int dyn = (int)(v->fn ? v->lds + c.lds_bytes : c.lds_bytes);
+  int nb = 0;
+  hipError_t e = v->fn ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, v->fn, v->threads, dyn)
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, gemm_skinny_kernel,
+                                                                      v->threads, dyn);
+  if (e != hipSuccess) return OCC_EHIP;
+  plan->wg_per_cu = nb;
+  return OCC_OK;
+}
+
+int gemm_launch(const GemmCall &c, hipStream_t s) {
+  occ_gemm_plan p;
+  int st = gemm_plan(c, &p);
+  if (st != OCC_OK) return st;
+  if (c.M == 0 || c.N == 0) return OCC_OK;
+  const Variant *v = find_variant(p.kernel_id);
+  const uint16_t *A = static_cast<const uint16_t *>(c.A);
+  const uint16_t *B = static_cast<const uint16_t *>(c.B);
+  uint16_t *C = static_cast<uint16_t *>(c.C);
+  if (v->fn) {
+    int dyn = v->lds + (int)c.lds_bytes;
+    static bool attr_set[16] = {};
+    if (!attr_set[v->id]) {
+      if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->fn),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              p.max_lds_per_wg) != hipSuccess)
+        return OCC_EHIP;
+      attr_set[v->id] = true;
+    }
+    int tiles_m = ceil_div(c.M, v->bm), tiles_n = ceil_div(c.N, v->bn);
+    hipLaunchKernelGGL(v->fn, dim3(p.grid), dim3(v->threads), dyn, s, A, B, C, c.M, c.N, c.K,
+                       tiles_m, tiles_n, c.stamps);
+  } else {
+    static bool attr_set_skinny = false;
+    if (!attr_set_skinny) {
+      if (hipFuncSetAttribute(reinterpret_cast<const void *>(gemm_skinny_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                              p.max_lds_per_wg - kSkinnyStaticLds) != hipSuccess)
+        return OCC_EHIP;
+      attr_set_skinny = true;
+    }
+    hipLaunchKernelGGL(gemm_skinny_kernel, dim3(p.grid), dim3(256), (int)c.lds_bytes, s, A, B, C,
+                       c.M, c.N, c.K, c.stamps);
+  }
+  return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
+}
+
+}  // namespace occ

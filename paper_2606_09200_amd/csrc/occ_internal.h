@@ -1,0 +1,76 @@
+// Internal interfaces of the occ library (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/occ.h"
+
+namespace occ {
+
+constexpr int kMaxReduceChunks = 64;
+constexpr int kMaxPermuteChunks = 512;
+
+// Per-device facts the launch plans depend on (queried once per device).
+struct DeviceInfo {
+  int ok;
+  int num_cus;
+  int lds_per_cu;       // bytes
+  int max_lds_per_wg;   // bytes
+  int clock_khz;
+  int gfx950;
+};
+const DeviceInfo &device_info(int device);
+int current_device_info(const DeviceInfo **out);
+
+// ---- GEMM ----------------------------------------------------------------
+struct GemmCall {
+  const void *A;
+  const void *B;
+  void *C;
+  int M, N, K;
+  size_t lds_bytes;
+  int grid_cap;         // 0 = one workgroup per tile
+  int variant;          // 0 = automatic, else a kernel variant id
+  uint64_t *stamps;     // optional [start, end] pair (atomic min/max), may be null
+};
+int gemm_plan(const GemmCall &c, occ_gemm_plan *plan);
+int gemm_launch(const GemmCall &c, hipStream_t s);
+
+// ---- communication-side kernels -----------------------------------------
+struct ReduceCall {
+  const float *const *bufs;  // host array
+  int nchunks;
+  size_t len;
+  float *out;
+  int wgs;                   // 0 = default
+  int priority;              // 0..3
+  uint64_t *stamps;
+};
+int reduce_launch(const ReduceCall &c, hipStream_t s);
+int reduce_default_wgs(const ReduceCall &c);
+
+struct PermuteCall {
+  const void *src;
+  void *dst;
+  const int32_t *perm;       // host array
+  int nchunks;
+  size_t chunk_bytes;
+  int wgs;
+  int priority;
+  uint64_t *stamps;
+};
+int permute_launch(const PermuteCall &c, hipStream_t s);
+int permute_default_wgs(const PermuteCall &c);
+
+// ---- validation (host only, no HIP calls) --------------------------------
+int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K);
+int validate_reduce(const float *const *bufs, int nchunks, size_t len, const float *out);
+int validate_permute(const void *src, const void *dst, const int32_t *perm, int nchunks,
+                     size_t chunk_bytes);
+
+// Timeline helper: sets n [start, end] pairs to [UINT64_MAX, 0].
+int stamps_reset(uint64_t *stamps, int npairs, hipStream_t s);
+
+}  // namespace occ

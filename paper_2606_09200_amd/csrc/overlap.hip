@@ -1,0 +1,262 @@
+// Two-stream launcher: sequential vs overlapped schedule of n_iter
+// GEMM -> collective iterations (Section 3.2, Fig. 1).
+//
+//   SEQ: one stream, G0 C0 G1 C1 ... G_{n-1} C_{n-1}.
+//   OVL: G_i on the compute stream; an event recorded after G_i is waited on
+//        by the comm stream before C_i (K_g^i -> K_c^i, Section 3.3), so
+//        G_{i+1} may run while C_i does.  The collective's precedence over
+//        later GEMMs is the comm kernel's wave priority (s_setprio); both
+//        streams keep the default queue priority.
+//   ISO: SEQ with an event between every two kernels, giving the mean
+//        duration of one GEMM and of one collective launch.
+//
+// Makespans are GPU event intervals.  The protocol follows Section 4.1:
+// `warmup` untimed repetitions, then the mean over `reps` timed ones.
+#include "occ_internal.h"
+
+#include <string.h>
+
+#include <vector>
+
+namespace occ {
+
+namespace {
+
+struct StreamPair {
+  hipStream_t comp = nullptr;
+  hipStream_t comm = nullptr;
+};
+StreamPair g_streams[64];
+
+int stream_pair(StreamPair **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OCC_ENODEV;
+  StreamPair &p = g_streams[dev];
+  if (p.comp == nullptr) {
+    if (hipStreamCreateWithFlags(&p.comp, hipStreamNonBlocking) != hipSuccess) return OCC_EHIP;
+    if (hipStreamCreateWithFlags(&p.comm, hipStreamNonBlocking) != hipSuccess) return OCC_EHIP;
+  }
+  *out = &p;
+  return OCC_OK;
+}
+
+struct Events {
+  std::vector<hipEvent_t> ev;
+  ~Events() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+  int make(int n, unsigned flags) {
+    ev.assign(n, nullptr);
+    for (int i = 0; i < n; ++i)
+      if (hipEventCreateWithFlags(&ev[i], flags) != hipSuccess) return OCC_EHIP;
+    return OCC_OK;
+  }
+};
+
+#define OCC_TRY(x)                 \
+  do {                             \
+    int st_ = (x);                 \
+    if (st_ != OCC_OK) return st_; \
+  } while (0)
+#define OCC_HIP(x)                                   \
+  do {                                               \
+    if ((x) != hipSuccess) return OCC_EHIP;          \
+  } while (0)
+
+struct Launcher {
+  GemmCall g;
+  ReduceCall r;
+  PermuteCall p;
+  int kind;
+
+  int gemm(hipStream_t s, uint64_t *stamps) {
+    GemmCall c = g;
+    c.stamps = stamps;
+    return gemm_launch(c, s);
+  }
+  int comm(hipStream_t s, uint64_t *stamps) {
+    if (kind == OCC_COMM_REDUCE) {
+      ReduceCall c = r;
+      c.stamps = stamps;
+      return reduce_launch(c, s);
+    }
+    PermuteCall c = p;
+    c.stamps = stamps;
+    return permute_launch(c, s);
+  }
+};
+
+int validate_cfg(const occ_overlap_cfg *c) {
+  if (c == nullptr) return OCC_EINVAL;
+  if (c->n_iter < 1 || c->reps < 1 || c->warmup < 0) return OCC_EINVAL;
+  if (c->comm_priority < 0 || c->comm_priority > 3 || c->comm_wgs < 0) return OCC_EINVAL;
+  if (c->gemm_grid < 0 || c->gemm_variant < 0) return OCC_EINVAL;
+  if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) != 0) return OCC_EINVAL;
+  OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K));
+  size_t cbytes = (size_t)c->M * c->N * 2;
+  // K_g writes C while K_c runs: C must not overlap anything K_c touches,
+  // and K_c's output must not overlap A or B.
+  auto hit = [](const void *a, size_t an, const void *b, size_t bn) {
+    if (!a || !b || !an || !bn) return false;
+    uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+    return a0 < b0 + bn && b0 < a0 + an;
+  };
+  size_t abytes = (size_t)c->M * c->K * 2, bbytes = (size_t)c->N * c->K * 2;
+  if (c->comm_kind == OCC_COMM_REDUCE) {
+    OCC_TRY(validate_reduce(c->bufs, c->nchunks, c->len, c->out));
+    size_t lb = c->len * 4;
+    for (int i = 0; i < c->nchunks; ++i)
+      if (hit(c->C, cbytes, c->bufs[i], lb)) return OCC_EALIAS;
+    if (hit(c->C, cbytes, c->out, lb) || hit(c->out, lb, c->A, abytes) || hit(c->out, lb, c->B, bbytes))
+      return OCC_EALIAS;
+  } else if (c->comm_kind == OCC_COMM_PERMUTE) {
+    OCC_TRY(validate_permute(c->src, c->dst, c->perm, c->nchunks, c->chunk_bytes));
+    size_t tb = c->chunk_bytes * (size_t)c->nchunks;
+    if (hit(c->C, cbytes, c->src, tb) || hit(c->C, cbytes, c->dst, tb) || hit(c->dst, tb, c->A, abytes) ||
+        hit(c->dst, tb, c->B, bbytes))
+      return OCC_EALIAS;
+  } else {
+    return OCC_EINVAL;
+  }
+  return OCC_OK;
+}
+
+}  // namespace
+
+int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
+  if (res == nullptr) return OCC_EINVAL;
+  OCC_TRY(validate_cfg(cfg));
+  memset(res, 0, sizeof *res);
+  const occ_overlap_cfg &c = *cfg;
+  const int flags = c.flags ? c.flags : (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO);
+  const int n = c.n_iter;
+
+  Launcher L;
+  L.kind = c.comm_kind;
+  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant, nullptr};
+  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, nullptr};
+  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, nullptr};
+
+  occ_gemm_plan plan;
+  OCC_TRY(gemm_plan(L.g, &plan));
+  res->gemm_wg_per_cu = plan.wg_per_cu;
+  res->gemm_grid = plan.grid;
+  res->gemm_tile_lds = plan.tile_lds_bytes;
+  res->comm_wgs = c.comm_wgs > 0 ? c.comm_wgs
+                  : (c.comm_kind == OCC_COMM_REDUCE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
+
+  StreamPair *sp = nullptr;
+  OCC_TRY(stream_pair(&sp));
+  hipStream_t s0 = sp->comp, s1 = sp->comm;
+
+  Events timing, deps;
+  OCC_TRY(timing.make(2 * n + 5, hipEventDefault));
+  OCC_TRY(deps.make(n, hipEventDisableTiming));
+  hipEvent_t *ev = timing.ev.data();
+  hipEvent_t *iso = ev + 4;  // 2n+1 boundaries of the isolated pass
+
+  double seq_sum = 0, ovl_sum = 0, seq_min = 1e300, ovl_min = 1e300, g_sum = 0, c_sum = 0;
+  int st = OCC_OK;
+  for (int rep = 0; rep < c.warmup + c.reps && st == OCC_OK; ++rep) {
+    const bool timed = rep >= c.warmup;
+    if (flags & OCC_RUN_SEQ) {
+      OCC_HIP(hipEventRecord(ev[0], s0));
+      for (int i = 0; i < n && st == OCC_OK; ++i) {
+        st = L.gemm(s0, nullptr);
+        if (st == OCC_OK) st = L.comm(s0, nullptr);
+      }
+      OCC_HIP(hipEventRecord(ev[1], s0));
+      OCC_HIP(hipEventSynchronize(ev[1]));
+      if (st != OCC_OK) break;
+      float ms = 0;
+      OCC_HIP(hipEventElapsedTime(&ms, ev[0], ev[1]));
+      if (timed) {
+        seq_sum += ms;
+        seq_min = ms < seq_min ? ms : seq_min;
+      }
+    }
+    if (flags & OCC_RUN_OVL) {
+      OCC_HIP(hipEventRecord(ev[2], s0));
+      OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
+      for (int i = 0; i < n && st == OCC_OK; ++i) {
+        st = L.gemm(s0, nullptr);
+        if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
+        if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
+        if (st == OCC_OK) st = L.comm(s1, nullptr);
+      }
+      // C_{n-1} waits on G_{n-1}, the last kernel of the compute stream, so
+      // the comm stream's end marks the end of the whole schedule.
+      OCC_HIP(hipEventRecord(ev[3], s1));
+      OCC_HIP(hipEventSynchronize(ev[3]));
+      if (st != OCC_OK) break;
+      float ms = 0;
+      OCC_HIP(hipEventElapsedTime(&ms, ev[2], ev[3]));
+      if (timed) {
+        ovl_sum += ms;
+        ovl_min = ms < ovl_min ? ms : ovl_min;
+      }
+    }
+    if (flags & OCC_RUN_ISO) {
+      OCC_HIP(hipEventRecord(iso[0], s0));
+      for (int i = 0; i < n && st == OCC_OK; ++i) {
+        st = L.gemm(s0, nullptr);
+        if (st == OCC_OK && hipEventRecord(iso[2 * i + 1], s0) != hipSuccess) st = OCC_EHIP;
+        if (st == OCC_OK) st = L.comm(s0, nullptr);
+        if (st == OCC_OK && hipEventRecord(iso[2 * i + 2], s0) != hipSuccess) st = OCC_EHIP;
+      }
+      OCC_HIP(hipEventSynchronize(iso[2 * n]));
+      if (st != OCC_OK) break;
+      if (timed) {
+        for (int i = 0; i < n; ++i) {
+          float a = 0, b = 0;
+          OCC_HIP(hipEventElapsedTime(&a, iso[2 * i], iso[2 * i + 1]));
+          OCC_HIP(hipEventElapsedTime(&b, iso[2 * i + 1], iso[2 * i + 2]));
+          g_sum += a;
+          c_sum += b;
+        }
+      }
+    }
+  }
+  if (st != OCC_OK) {
+    (void)hipStreamSynchronize(s0);
+    (void)hipStreamSynchronize(s1);
+    return st;
+  }
+
+  // Timeline: one more, untimed, overlapped repetition with every kernel
+  // stamping its first-start / last-end clock.
+  if (c.timeline != nullptr) {
+    OCC_TRY(stamps_reset(c.timeline, 2 * n, s0));
+    OCC_HIP(hipEventRecord(ev[2], s0));
+    OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
+    for (int i = 0; i < n && st == OCC_OK; ++i) {
+      st = L.gemm(s0, c.timeline + 4 * i);
+      if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
+      if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
+      if (st == OCC_OK) st = L.comm(s1, c.timeline + 4 * i + 2);
+    }
+    OCC_HIP(hipEventRecord(ev[3], s1));
+    OCC_HIP(hipEventSynchronize(ev[3]));
+    if (st != OCC_OK) return st;
+  }
+
+  const double R = c.reps;
+  if (flags & OCC_RUN_SEQ) {
+    res->t_seq_ms = seq_sum / R;
+    res->t_seq_min_ms = seq_min;
+  }
+  if (flags & OCC_RUN_OVL) {
+    res->t_ovl_ms = ovl_sum / R;
+    res->t_ovl_min_ms = ovl_min;
+  }
+  if ((flags & OCC_RUN_SEQ) && (flags & OCC_RUN_OVL) && res->t_seq_ms > 0)
+    res->reduction_pct = 100.0 * (1.0 - res->t_ovl_ms / res->t_seq_ms);
+  if (flags & OCC_RUN_ISO) {
+    res->t_gemm_ms = g_sum / (R * n);
+    res->t_comm_ms = c_sum / (R * n);
+  }
+  return OCC_OK;
+}
+
+}  // namespace occ

@@ -1,0 +1,115 @@
+"""CPU checks of the C ABI: the library loads, exports every declared entry
+point, and rejects bad arguments with the documented status before touching
+the GPU (no kernel is launched and no device memory is read here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "occ.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2606_09200_amd import binding
+    return binding.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for f in ("occ_gemm", "share_reduce", "share_permute", "run_overlap", "occ_strerror"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    missing = [f for f in declared_functions() if not hasattr(L, f)]
+    assert not missing, missing
+
+
+def test_strerror_and_version(L):
+    from paper_2606_09200_amd import binding
+    for code in range(0, -7, -1):
+        assert binding.occ_strerror(code).startswith("OCC_")
+    assert "unknown" in binding.occ_strerror(-99)
+    assert binding.occ_version() == (1, 0)
+
+
+P = ctypes.c_void_p
+
+
+def test_gemm_argument_errors(L):
+    # bad sizes, K not a multiple of 8, null or misaligned pointers, aliasing
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), -1, 4, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), 4, 4, 12, 0, None) == -1
+    assert L.occ_gemm(None, P(0x2000), P(0x3000), 4, 4, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1008), P(0x2000), P(0x3000), 4, 4, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x1010), 4, 4, 8, 0, None) == -4  # C inside A
+    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, -1, 0, None) == -1
+    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, 0, -5, None) == -1
+
+
+def test_reduce_argument_errors(L):
+    arr = (ctypes.c_void_p * 65)(*([0x10000 * (i + 1) for i in range(65)]))
+    out = P(0x900000)
+    assert L.share_reduce(arr, 0, 16, out, None) == -1
+    assert L.share_reduce(arr, 65, 16, out, None) == -1
+    assert L.share_reduce(None, 2, 16, out, None) == -1
+    assert L.share_reduce(arr, 2, 16, None, None) == -1
+    assert L.share_reduce(arr, 2, 16, P(0x10000 + 8), None) == -4      # out overlaps chunk 0
+    nul = (ctypes.c_void_p * 2)(0x10000, 0)
+    assert L.share_reduce(nul, 2, 16, out, None) == -1
+    odd = (ctypes.c_void_p * 2)(0x10002, 0x20000)
+    assert L.share_reduce(odd, 2, 16, out, None) == -1                # not 4-byte aligned
+    assert L.share_reduce_ex(arr, 2, 16, out, 0, 4, None) == -1       # priority out of range
+    assert L.share_reduce_ex(arr, 2, 16, out, -1, 0, None) == -1
+
+
+def test_permute_argument_errors(L):
+    perm = (ctypes.c_int32 * 4)(0, 2, 2, 3)
+    assert L.share_permute(P(0x1000), P(0x100000), perm, 4, 64, None) == -3
+    perm = (ctypes.c_int32 * 4)(0, 1, 4, 3)
+    assert L.share_permute(P(0x1000), P(0x100000), perm, 4, 64, None) == -3
+    perm = (ctypes.c_int32 * 4)(3, 1, 0, 2)
+    assert L.share_permute(P(0x1000), P(0x1000 + 128), perm, 4, 64, None) == -4
+    assert L.share_permute(None, P(0x100000), perm, 4, 64, None) == -1
+    assert L.share_permute(P(0x1000), P(0x100000), None, 4, 64, None) == -1
+    assert L.share_permute(P(0x1000), P(0x100000), perm, 0, 64, None) == -1
+    assert L.share_permute(P(0x1000), P(0x100000), perm, 513, 64, None) == -1
+
+
+def test_run_overlap_argument_errors(L):
+    from paper_2606_09200_amd import binding as b
+    cfg = b.occ_overlap_cfg()
+    res = b.occ_overlap_result()
+    assert L.run_overlap(None, ctypes.byref(res)) == -1
+    assert L.run_overlap(ctypes.byref(cfg), None) == -1
+    cfg.M = cfg.N = cfg.K = 8
+    cfg.A, cfg.B, cfg.C = 0x1000, 0x2000, 0x3000
+    arr = (ctypes.c_void_p * 2)(0x10000, 0x20000)
+    cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    cfg.nchunks, cfg.len, cfg.out = 2, 64, 0x30000
+    cfg.n_iter, cfg.reps, cfg.warmup = 0, 1, 0
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1   # n_iter < 1
+    cfg.n_iter = 2
+    cfg.comm_priority = 7
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.comm_priority = 3
+    cfg.comm_kind = 5
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.comm_kind = 0
+    cfg.out = 0x3000 + 16                                                 # comm output inside C
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
+    cfg.out = 0x30000
+    arr2 = (ctypes.c_void_p * 2)(0x10000, 0x3000)                         # C is a comm input
+    cfg.bufs = ctypes.cast(arr2, ctypes.POINTER(ctypes.c_void_p))
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
+    cfg.flags = 64
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1

@@ -1,0 +1,155 @@
+"""Parity of the communication-side kernels (through the C ABI) with the oracle:
+bit-exact for the fixed-order chunk sum and for the chunk permutation."""
+import os
+import struct
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_09200_amd import binding as occ
+from paper_2606_09200_amd import inputs
+from gpu_common import DEV
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gpu_reduce(chunks_host, offset=0, wgs=0, priority=0):
+    """Run share_reduce on copies of the rows of chunks_host, optionally
+    placed `offset` floats into their buffers (to exercise misalignment)."""
+    n, length = chunks_host.shape
+    store = torch.zeros((n, length + offset + 4), dtype=torch.float32, device=DEV)
+    store[:, offset:offset + length] = torch.from_numpy(np.ascontiguousarray(chunks_host)).to(DEV)
+    bufs = [store[i, offset:offset + length] for i in range(n)]
+    out_store = torch.full((length + offset + 4,), float("nan"), dtype=torch.float32, device=DEV)
+    out = out_store[offset:offset + length]
+    occ.share_reduce(bufs, out, wgs=wgs, priority=priority)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def u32(x):
+    return np.asarray(x, dtype=np.float32).view(np.uint32)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 8, 9, 16, 17, 64])
+@pytest.mark.parametrize("length", [1, 3, 4, 1000, 65539])
+def test_reduce_bit_exact(n, length):
+    c = inputs.reduce_chunks(n, length, seed=n * 1000 + length).numpy()
+    assert np.array_equal(u32(gpu_reduce(c)), u32(oracle.chunk_sum_f32(c)))
+
+
+@pytest.mark.parametrize("offset", [1, 2, 3])
+def test_reduce_misaligned_bit_exact(offset):
+    c = inputs.reduce_chunks(8, 4099, seed=offset).numpy()
+    assert np.array_equal(u32(gpu_reduce(c, offset=offset)), u32(oracle.chunk_sum_f32(c)))
+
+
+def test_reduce_order_probes():
+    with open(os.path.join(GOLDEN, "chunk_sum_order.txt")) as f:
+        rows = [l.split("|") for l in f if l.strip() and not l.startswith("#")]
+    for row in rows:
+        vals = [eval(v) for v in row[0].split(",")]
+        # 4100 copies so that both the vector body and the scalar tail see the probe
+        c = np.repeat(np.array(vals, dtype=np.float32)[:, None], 4101, axis=1)
+        got = u32(gpu_reduce(c))
+        assert np.all(got == int(row[1], 16)), row[0]
+
+
+def test_reduce_mixed_magnitudes_and_subnormals():
+    rng = np.random.default_rng(9)
+    c = (rng.standard_normal((8, 20000)) * np.float32(2.0) ** rng.integers(-140, 100, size=(8, 20000))).astype(np.float32)
+    c[3, ::7] = np.float32(1e-45)           # smallest subnormal
+    c[5, ::11] = -c[0, ::11]                # exact cancellations
+    assert np.array_equal(u32(gpu_reduce(c)), u32(oracle.chunk_sum_f32(c)))
+
+
+def test_reduce_all_ones_and_integers():
+    assert np.all(gpu_reduce(np.ones((8, 5000), dtype=np.float32)) == 8.0)
+    ci = np.random.default_rng(4).integers(-1024, 1025, size=(8, 5000))
+    assert np.array_equal(gpu_reduce(ci.astype(np.float32)), ci.sum(axis=0).astype(np.float32))
+
+
+@pytest.mark.parametrize("wgs,priority", [(1, 0), (3, 3), (1000, 1), (0, 2)])
+def test_reduce_knobs_do_not_change_bits(wgs, priority):
+    c = inputs.reduce_chunks(8, 300001, seed=2).numpy()
+    assert np.array_equal(u32(gpu_reduce(c, wgs=wgs, priority=priority)), u32(oracle.chunk_sum_f32(c)))
+
+
+def test_reduce_empty_is_noop():
+    out = torch.full((4,), 7.0, device=DEV)
+    bufs = [torch.zeros(4, device=DEV)[:0]]
+    occ.lib().share_reduce((occ.ctypes.c_void_p * 1)(bufs[0].data_ptr()), 1, 0, occ._ptr(out), occ._stream(None))
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mb", "cb"])
+def test_reduce_workload_sizes_bit_exact(name):
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS[name]
+    chunks = inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=DEV)
+    out = torch.empty(w.length, device=DEV)
+    occ.share_reduce(chunks, out)
+    torch.cuda.synchronize()
+    ref = oracle.chunk_sum_f32(chunks.cpu().numpy())
+    assert np.array_equal(u32(out.cpu().numpy()), u32(ref))
+
+
+# ----------------------------------------------------------------- permutation
+def gpu_permute(src_host, perm, chunk_bytes, byte_offset=0, wgs=0, priority=0):
+    total = src_host.size
+    s = torch.zeros(total + 64, dtype=torch.uint8, device=DEV)
+    s[byte_offset:byte_offset + total] = torch.from_numpy(src_host).to(DEV)
+    d = torch.zeros(total + 64, dtype=torch.uint8, device=DEV)
+    occ.share_permute(s[byte_offset:byte_offset + total], d[byte_offset:byte_offset + total], perm,
+                      chunk_bytes, wgs=wgs, priority=priority)
+    torch.cuda.synchronize()
+    return d[byte_offset:byte_offset + total].cpu().numpy()
+
+
+@pytest.mark.parametrize("n,cb", [(1, 16), (4, 4096), (64, 65536), (7, 1040), (512, 48), (3, 1001), (5, 17)])
+def test_permute_bit_exact(n, cb):
+    src = inputs.permute_payload(n, cb, seed=n + cb).numpy()
+    perm = inputs.chunk_permutation(n, seed=n)
+    want = oracle.permute_chunks(src, perm.numpy(), cb)
+    assert np.array_equal(gpu_permute(src, perm, cb), want)
+
+
+@pytest.mark.parametrize("offset", [1, 8])
+def test_permute_misaligned_bit_exact(offset):
+    src = inputs.permute_payload(6, 4096, seed=offset).numpy()
+    perm = inputs.chunk_permutation(6, seed=offset)
+    want = oracle.permute_chunks(src, perm.numpy(), 4096)
+    assert np.array_equal(gpu_permute(src, perm, 4096, byte_offset=offset), want)
+
+
+def test_permute_identity_and_round_trip():
+    src = inputs.permute_payload(32, 8192, seed=5).numpy()
+    ident = list(range(32))
+    assert np.array_equal(gpu_permute(src, ident, 8192), src)
+    p = inputs.chunk_permutation(32, seed=6).numpy()
+    once = gpu_permute(src, p, 8192)
+    assert np.array_equal(gpu_permute(once, np.argsort(p), 8192), src)
+
+
+@pytest.mark.parametrize("wgs,priority", [(1, 3), (7, 0), (4096, 2)])
+def test_permute_knobs_do_not_change_bits(wgs, priority):
+    src = inputs.permute_payload(16, 1 << 16, seed=8).numpy()
+    perm = inputs.chunk_permutation(16, seed=8)
+    want = oracle.permute_chunks(src, perm.numpy(), 1 << 16)
+    assert np.array_equal(gpu_permute(src, perm, 1 << 16, wgs=wgs, priority=priority), want)
+
+
+def test_permute_workload_size_bit_exact():
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS["a2a"]
+    src = inputs.permute_payload(w.nchunks, w.chunk_bytes, seed=2, device=DEV)
+    perm = inputs.chunk_permutation(w.nchunks, seed=3)
+    dst = torch.empty_like(src)
+    occ.share_permute(src, dst, perm, w.chunk_bytes)
+    torch.cuda.synchronize()
+    want = oracle.permute_chunks(src.cpu().numpy(), perm.numpy(), w.chunk_bytes)
+    assert np.array_equal(dst.cpu().numpy(), want)

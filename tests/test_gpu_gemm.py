@@ -1,0 +1,153 @@
+"""GEMM parity: the HIP kernels (through the C ABI) against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_09200_amd import binding as occ
+from paper_2606_09200_amd import inputs
+from gpu_common import DEV, assert_gemm_close, bf16_bits, sample_tiles
+
+pytestmark = pytest.mark.gpu
+
+TILED = [1, 2, 3, 4, 5, 6, 7, 9]
+
+
+def run_gemm(A, B, lds_bytes=0, variant=0, grid_cap=0):
+    M, K = A.shape
+    N = B.shape[0]
+    Ad, Bd = A.to(DEV), B.to(DEV)
+    C = torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm_ex(Ad, Bd, C, lds_bytes=lds_bytes, variant=variant, grid_cap=grid_cap)
+    torch.cuda.synchronize()
+    return bf16_bits(C)
+
+
+def int_operands(M, N, K, seed):
+    g = torch.Generator().manual_seed(seed)
+    A = torch.randint(-2, 3, (M, K), generator=g).to(torch.bfloat16)
+    B = torch.randint(-2, 3, (N, K), generator=g).to(torch.bfloat16)
+    return A, B
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 512, 512), (300, 200, 136), (1, 1, 8), (17, 33, 64),
+                                   (257, 129, 520), (64, 64, 32), (16, 1000, 1032), (5, 77, 256)])
+def test_gemm_auto_full_parity(M, N, K):
+    A, B = inputs.gemm_operands(M, N, K, seed=0)
+    got = run_gemm(A, B)
+    ref = oracle.gemm_bf16(A, B, M, N, K)
+    frac = assert_gemm_close(got, ref, 1.0, 1.0, K, "auto %dx%dx%d" % (M, N, K))
+    assert frac < 0.05
+
+
+@pytest.mark.parametrize("variant", TILED + [8])
+def test_gemm_every_variant_ragged(variant):
+    M = 16 if variant == 8 else 300
+    N, K = 260, 200
+    A, B = inputs.gemm_operands(M, N, K, seed=variant)
+    got = run_gemm(A, B, variant=variant)
+    ref = oracle.gemm_bf16(A, B, M, N, K)
+    assert_gemm_close(got, ref, 1.0, 1.0, K, "variant %d" % variant)
+
+
+@pytest.mark.parametrize("variant", TILED + [8])
+def test_gemm_integer_operands_bit_exact(variant):
+    # sums of products of {-2..2} are exact in fp32 in any order: bit-exact
+    M = 13 if variant == 8 else 197
+    A, B = int_operands(M, 150, 512, seed=variant)
+    got = run_gemm(A, B, variant=variant)
+    assert np.array_equal(got, oracle.gemm_bf16(A, B, M, 150, 512))
+
+
+def test_gemm_identity_and_ones():
+    A, _ = inputs.gemm_operands(96, 8, 128, seed=3)
+    eye = torch.eye(128).to(torch.bfloat16)
+    assert np.array_equal(run_gemm(A, eye), bf16_bits(A))
+    ones_a = torch.ones((40, 512), dtype=torch.bfloat16)
+    ones_b = torch.ones((24, 512), dtype=torch.bfloat16)
+    assert np.all(run_gemm(ones_a, ones_b) == 0x4400)
+
+
+def test_gemm_tiled_variants_agree_bitwise():
+    A, B = inputs.gemm_operands(384, 320, 448, seed=11)
+    base = run_gemm(A, B, variant=1)
+    for v in TILED[1:]:
+        assert np.array_equal(run_gemm(A, B, variant=v), base), v
+
+
+@pytest.mark.parametrize("variant", [0, 1, 5, 7, 8])
+def test_gemm_pad_and_grid_cap_do_not_change_result(variant):
+    M = 16 if variant == 8 else 520
+    A, B = inputs.gemm_operands(M, 384, 256, seed=5)
+    base = run_gemm(A, B, variant=variant)
+    for pad in (16 << 10, 64 << 10):
+        plan = occ.occ_gemm_plan_query(M, 384, 256, pad, variant)
+        if plan["feasible"]:
+            assert np.array_equal(run_gemm(A, B, lds_bytes=pad, variant=variant), base), pad
+    for cap in (1, 7, 256):
+        assert np.array_equal(run_gemm(A, B, variant=variant, grid_cap=cap), base), cap
+
+
+def test_gemm_empty_and_zero_k():
+    A = torch.zeros((0, 64), dtype=torch.bfloat16)
+    B = torch.zeros((32, 64), dtype=torch.bfloat16)
+    assert run_gemm(A, B).shape == (0, 32)
+    A = torch.zeros((20, 0), dtype=torch.bfloat16)
+    B = torch.zeros((30, 0), dtype=torch.bfloat16)
+    Ad = torch.zeros((20, 8), dtype=torch.bfloat16, device=DEV)[:, :0]
+    C = torch.full((20, 30), 1.0, device=DEV, dtype=torch.bfloat16)
+    occ.lib().occ_gemm(occ._ptr(Ad), None, occ._ptr(C), 20, 30, 0, 0, occ._stream(None))
+    torch.cuda.synchronize()
+    assert np.all(bf16_bits(C) == 0)
+
+
+def test_gemm_rejects_infeasible_pad():
+    A, B = inputs.gemm_operands(256, 256, 64, seed=1)
+    plan = occ.occ_gemm_plan_query(256, 256, 64, 0, 1)
+    too_big = plan["max_lds_per_wg"] - plan["tile_lds_bytes"] + 16
+    C = torch.empty((256, 256), device=DEV, dtype=torch.bfloat16)
+    with pytest.raises(occ.OccError) as e:
+        occ.occ_gemm_ex(A.to(DEV), B.to(DEV), C, lds_bytes=too_big, variant=1)
+    assert e.value.status == occ.OCC_ELDS
+
+
+def test_occupancy_non_increasing_in_pad():
+    for variant in (0, 5, 6, 7):
+        prev = None
+        for pad_kib in (0, 16, 32, 64, 96, 128):
+            p = occ.occ_gemm_plan_query(8192, 8192, 8192, pad_kib << 10, variant)
+            w = p["wg_per_cu"] if p["feasible"] else 0
+            if prev is not None:
+                assert w <= prev
+            prev = w
+            if p["feasible"]:
+                # where LDS binds, residency is floor(LDS per CU / (S_tile + pad))
+                lds_bound = p["lds_per_cu"] // (p["tile_lds_bytes"] + (pad_kib << 10))
+                assert w <= lds_bound
+
+
+# ----------------------------------------------------------------- full sizes
+@pytest.mark.parametrize("name", ["cb", "a2a"])
+def test_gemm_full_size_sampled_tiles(name):
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS[name]
+    A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, device=DEV)
+    C = torch.empty((w.M, w.N), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm(A, B, C)
+    torch.cuda.synchronize()
+    Ah, Bh, Ch = bf16_bits(A), bf16_bits(B), bf16_bits(C)
+    for m0, n0 in sample_tiles(w.M, w.N):
+        m1, n1 = min(m0 + 64, w.M), min(n0 + 64, w.N)
+        ref = oracle.gemm_bf16(Ah, Bh, w.M, w.N, w.K, rows=(m0, m1), cols=(n0, n1))
+        assert_gemm_close(Ch[m0:m1, n0:n1], ref, 1.0, 1.0, w.K, "%s tile %d,%d" % (name, m0, n0))
+
+
+def test_gemm_full_size_skinny_full_parity():
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS["mb"]
+    A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=DEV)
+    C = torch.empty((w.M, w.N), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm(A, B, C)
+    torch.cuda.synchronize()
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), w.M, w.N, w.K)
+    assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full")

@@ -1,0 +1,102 @@
+"""The two-stream launcher: results, schedule semantics and timing sanity.
+
+Section 3.3: overlap keeps the dependency K_g^i -> K_c^i and therefore the
+results; the outputs after run_overlap must be bit-identical to one plain
+occ_gemm and one plain share_* call, for every pad and priority.  The kernel
+timeline recorded by the library must respect the schedule's orderings
+(checked with the oracle's definitions), and the makespans must satisfy the
+bounds the schedule implies.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import schedule
+from paper_2606_09200_amd import binding as occ
+from paper_2606_09200_amd import inputs
+from gpu_common import DEV, assert_gemm_close, bf16_bits
+
+pytestmark = pytest.mark.gpu
+
+
+def tiny_reduce_setup(M=512, N=512, K=512, nchunks=4, length=1 << 20):
+    A, B = inputs.gemm_operands(M, N, K, seed=0, device=DEV)
+    C = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    chunks = inputs.reduce_chunks(nchunks, length, seed=1, device=DEV)
+    out = torch.empty(length, device=DEV)
+    return A, B, C, chunks, out
+
+
+def timeline_intervals(tl, n):
+    t = tl.cpu().numpy().astype(np.int64).reshape(n, 4)
+    g = [(int(r[0]), int(r[1])) for r in t]
+    c = [(int(r[2]), int(r[3])) for r in t]
+    return g, c
+
+
+@pytest.mark.parametrize("pad,prio", [(0, 0), (0, 3), (64 << 10, 0), (64 << 10, 3)])
+def test_overlap_results_match_plain_calls(pad, prio):
+    A, B, C, chunks, out = tiny_reduce_setup()
+    C_ref = torch.empty_like(C)
+    out_ref = torch.empty_like(out)
+    occ.occ_gemm(A, B, C_ref)
+    occ.share_reduce(chunks, out_ref)
+    torch.cuda.synchronize()
+    r = occ.run_overlap(A, B, C, bufs=chunks, out=out, lds_bytes=pad, comm_priority=prio,
+                        n_iter=4, reps=2, warmup=1)
+    torch.cuda.synchronize()
+    assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
+    assert torch.equal(out.view(torch.int32), out_ref.view(torch.int32))
+    assert r["t_seq_ms"] > 0 and r["t_ovl_ms"] > 0 and r["t_gemm_ms"] > 0 and r["t_comm_ms"] > 0
+    # and both equal the oracle
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), 512, 512, 512)
+    assert_gemm_close(bf16_bits(C), ref, 1.0, 1.0, 512, "overlap C")
+    assert np.array_equal(out.cpu().numpy().view(np.uint32),
+                          oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
+
+
+def test_overlap_permute_results_match_plain_calls():
+    A, B = inputs.gemm_operands(1024, 768, 512, seed=0, device=DEV)
+    C = torch.empty((1024, 768), device=DEV, dtype=torch.bfloat16)
+    src = inputs.permute_payload(64, 1 << 16, seed=2, device=DEV)
+    dst = torch.empty_like(src)
+    perm = inputs.chunk_permutation(64, seed=3)
+    r = occ.run_overlap(A, B, C, src=src, dst=dst, perm=perm, chunk_bytes=1 << 16, n_iter=3,
+                        reps=2, warmup=1)
+    torch.cuda.synchronize()
+    want = oracle.permute_chunks(src.cpu().numpy(), perm.numpy(), 1 << 16)
+    assert np.array_equal(dst.cpu().numpy(), want)
+    assert r["t_ovl_ms"] > 0
+
+
+def test_overlap_timeline_respects_schedule():
+    n = 6
+    A, B, C, chunks, out = tiny_reduce_setup(M=2048, N=2048, K=2048, nchunks=8, length=1 << 22)
+    tl = torch.zeros(4 * n, dtype=torch.int64, device=DEV)
+    occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=n, reps=1, warmup=1, timeline=tl)
+    torch.cuda.synchronize()
+    g, c = timeline_intervals(tl, n)
+    assert all(e > s for s, e in g + c)
+    assert schedule.dependency_violations(g, c) == []
+    rate = schedule.overlap_rate(g, c)
+    assert 0.0 <= rate <= 1.0
+
+
+def test_makespan_bounds():
+    n = 8
+    A, B, C, chunks, out = tiny_reduce_setup(M=2048, N=2048, K=4096, nchunks=8, length=1 << 23)
+    r = occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=n, reps=3, warmup=2)
+    tg, tc = r["t_gemm_ms"], r["t_comm_ms"]
+    # sequential ~ n (t_g + t_c); overlap can be no faster than the busier
+    # stream alone and no slower than running everything back to back (+ slack)
+    assert r["t_seq_ms"] == pytest.approx(n * (tg + tc), rel=0.25)
+    assert r["t_ovl_ms"] >= 0.8 * n * max(tg, tc)
+    assert r["t_ovl_ms"] <= 1.25 * r["t_seq_ms"]
+    assert r["reduction_pct"] == pytest.approx(100 * (1 - r["t_ovl_ms"] / r["t_seq_ms"]))
+
+
+def test_plan_reports_occupancy_shaping():
+    r0 = occ.occ_gemm_plan_query(8192, 8192, 8192, 0, 5)
+    r1 = occ.occ_gemm_plan_query(8192, 8192, 8192, 96 << 10, 5)
+    assert r0["wg_per_cu"] >= r1["wg_per_cu"] >= 1
