@@ -364,7 +364,7 @@ int auto_variant(int M, int N, int K, int num_cus) {
   (void)K;
   if (M <= 16) return kSkinnyId;
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
-  if (big >= num_cus) return 1;
+  if (big >= num_cus) return 2;
   long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   if (mid >= num_cus / 2) return 5;
   return 7;

@@ -1,0 +1,64 @@
+"""Launch one kernel of a workload a few times, for hardware-counter runs.
+
+    python3 paper_2606_09200_amd/kernel_driver.py --workload cb --kernel gemm --launches 5
+
+Synchronises after every launch so that each dispatch is measured on its own,
+then (unless --no-copy) runs one plain device-to-device copy of --copy-mib MiB
+whose bytes are known exactly: the counter values it reads give the scale
+factor between the counters and true HBM bytes.
+"""
+import argparse
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+import torch  # noqa: E402
+
+from paper_2606_09200_amd import binding as occ  # noqa: E402
+from paper_2606_09200_amd import inputs  # noqa: E402
+from paper_2606_09200_amd.workloads import WORKLOADS  # noqa: E402
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", default="cb", choices=sorted(WORKLOADS))
+    ap.add_argument("--kernel", default="gemm", choices=["gemm", "comm"])
+    ap.add_argument("--launches", type=int, default=5)
+    ap.add_argument("--pad-kib", type=int, default=0)
+    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--copy-mib", type=int, default=1024)
+    ap.add_argument("--no-copy", action="store_true")
+    a = ap.parse_args(argv)
+    w = WORKLOADS[a.workload]
+    dev = "cuda:0"
+    if a.kernel == "gemm":
+        A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=dev)
+        C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
+        run = lambda: occ.occ_gemm_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
+    elif w.comm == "reduce":
+        ch = inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev)
+        out = torch.empty(w.length, device=dev)
+        run = lambda: occ.share_reduce(ch, out)
+    else:
+        src = inputs.permute_payload(w.nchunks, w.chunk_bytes, seed=2, device=dev)
+        dst = torch.empty_like(src)
+        perm = inputs.chunk_permutation(w.nchunks, seed=3)
+        run = lambda: occ.share_permute(src, dst, perm, w.chunk_bytes)
+    torch.cuda.synchronize()
+    for i in range(a.launches):
+        run()
+        torch.cuda.synchronize()
+        print("launch %d done" % i, flush=True)
+    if not a.no_copy:
+        x = torch.ones(a.copy_mib << 18, device=dev)   # float32: MiB * 2^18 elements
+        y = torch.empty_like(x)
+        torch.cuda.synchronize()
+        y.copy_(x)
+        torch.cuda.synchronize()
+        print("copy of %d MiB done (%d bytes read, %d written)" % (a.copy_mib, a.copy_mib << 20, a.copy_mib << 20), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
