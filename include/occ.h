@@ -172,6 +172,7 @@ typedef struct occ_overlap_cfg {
   size_t lds_bytes;         /* extra LDS per GEMM workgroup (Section 3.1) */
   int gemm_variant;         /* OCC_GEMM_* (0 = automatic) */
   int gemm_grid;            /* 0: one workgroup per tile; > 0: persistent grid cap */
+  int gemm_priority;        /* wave priority of the GEMM kernel, 0 (normal) .. 3 */
   /* K_c: as share_reduce (comm_kind 0) or share_permute (comm_kind 1) */
   int comm_kind;
   const float *const *bufs; /* host array of device pointers */
@@ -194,6 +195,15 @@ typedef struct occ_overlap_cfg {
      10 ns ticks of the GPU's constant-rate clock (earliest workgroup start,
      latest workgroup end).  NULL = no timeline. */
   uint64_t *timeline;
+  /* optional device buffer of 4 + 8*wg_trace_cap uint32: for that same
+     repetition, word 0 counts workgroups and record i (words 4+8i .. 11+8i)
+     is {tag, workgroup id, HW_ID, XCC_ID, t0 lo, t0 hi, t1 lo, t1 hi}: tag =
+     2*iteration (+1 for the collective), HW_ID/XCC_ID the hardware registers
+     naming the CU (bits 11:8), shader array (12), shader engine (15:13) and
+     XCD (3:0), t0/t1 the workgroup's start/end clock (10 ns ticks).  Records
+     beyond wg_trace_cap are counted but not written.  NULL = off. */
+  uint32_t *wg_trace;
+  int wg_trace_cap;
 } occ_overlap_cfg;
 
 typedef struct occ_overlap_result {

@@ -44,12 +44,14 @@ class occ_overlap_cfg(ctypes.Structure):
         ("M", ctypes.c_int), ("N", ctypes.c_int), ("K", ctypes.c_int),
         ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
         ("lds_bytes", ctypes.c_size_t), ("gemm_variant", ctypes.c_int), ("gemm_grid", ctypes.c_int),
+        ("gemm_priority", ctypes.c_int),
         ("comm_kind", ctypes.c_int), ("bufs", ctypes.POINTER(ctypes.c_void_p)),
         ("nchunks", ctypes.c_int), ("len", ctypes.c_size_t), ("out", ctypes.c_void_p),
         ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("perm", ctypes.POINTER(ctypes.c_int32)),
         ("chunk_bytes", ctypes.c_size_t), ("comm_wgs", ctypes.c_int), ("comm_priority", ctypes.c_int),
         ("n_iter", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
         ("flags", ctypes.c_int), ("timeline", ctypes.c_void_p),
+        ("wg_trace", ctypes.c_void_p), ("wg_trace_cap", ctypes.c_int),
     ]
 
 
@@ -206,14 +208,31 @@ def share_permute(src, dst, perm, chunk_bytes, stream=None, wgs=0, priority=0):
     return dst
 
 
+def decode_wg_trace(wg_trace):
+    """Records of a filled wg_trace tensor as a list of dicts (host side)."""
+    w = wg_trace.cpu().numpy().astype("int64") & 0xFFFFFFFF
+    n = min(int(w[0]), (w.size - 4) // 8)
+    out = []
+    for i in range(n):
+        r = w[4 + 8 * i: 12 + 8 * i]
+        hw, xcc = int(r[2]), int(r[3])
+        out.append({"tag": int(r[0]), "iter": int(r[0]) >> 1, "kind": "comm" if r[0] & 1 else "gemm",
+                    "block": int(r[1]), "cu": (hw >> 8) & 0xF, "sh": (hw >> 12) & 1,
+                    "se": (hw >> 13) & 0x7, "xcc": xcc & 0xF,
+                    "t0": int(r[4]) | (int(r[5]) << 32), "t1": int(r[6]) | (int(r[7]) << 32)})
+    return out
+
+
 def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
-                lds_bytes=0, gemm_variant=0, gemm_grid=0, comm_wgs=0, comm_priority=3, n_iter=10,
-                reps=20, warmup=10, flags=0, timeline=None):
+                lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0, comm_priority=3,
+                n_iter=10,
+                reps=20, warmup=10, flags=0, timeline=None, wg_trace=None):
     """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
 
     Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
     ``chunk_bytes`` for the alltoall share.  ``timeline``: optional uint64 GPU
-    tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).
+    tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
+    optional int32 GPU tensor of 4 + 8*cap entries (see occ_overlap_cfg.wg_trace).
     Returns the occ_overlap_result fields as a dict.
     """
     M, N, K = _gemm_args(A, B, C)
@@ -221,6 +240,7 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
     cfg.M, cfg.N, cfg.K = M, N, K
     cfg.A, cfg.B, cfg.C = _ptr(A).value, _ptr(B).value, _ptr(C).value
     cfg.lds_bytes, cfg.gemm_variant, cfg.gemm_grid = int(lds_bytes), int(gemm_variant), int(gemm_grid)
+    cfg.gemm_priority = int(gemm_priority)
     keep = []
     if bufs is not None:
         arr, n, length = _chunk_ptrs(bufs)
@@ -246,6 +266,11 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
         if timeline.dtype not in (torch.int64, torch.uint64) or timeline.numel() < 4 * n_iter:
             raise ValueError("timeline must hold 4*n_iter 64-bit entries")
         cfg.timeline = timeline.data_ptr()
+    if wg_trace is not None:
+        if wg_trace.dtype not in (torch.int32, torch.uint32) or wg_trace.numel() < 12:
+            raise ValueError("wg_trace must be a 32-bit tensor of 4 + 8*cap entries")
+        cfg.wg_trace = wg_trace.data_ptr()
+        cfg.wg_trace_cap = (wg_trace.numel() - 4) // 8
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}

@@ -96,7 +96,7 @@ int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size
   int st = occ::validate_gemm(A, B, C, M, N, K);
   if (st != OCC_OK) return st;
   if (grid_cap < 0 || variant < 0) return OCC_EINVAL;
-  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, nullptr};
+  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}};
   return occ::gemm_launch(c, static_cast<hipStream_t>(stream));
 }
 
@@ -109,7 +109,7 @@ int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int 
                         occ_gemm_plan *plan) {
   if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
   memset(plan, 0, sizeof *plan);
-  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, nullptr};
+  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}};
   return occ::gemm_plan(c, plan);
 }
 
@@ -120,7 +120,7 @@ int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *ou
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (len > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, nullptr};
+  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}};
   return occ::reduce_launch(c, static_cast<hipStream_t>(stream));
 }
 
@@ -135,7 +135,7 @@ int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunk
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (chunk_bytes > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, nullptr};
+  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}};
   return occ::permute_launch(c, static_cast<hipStream_t>(stream));
 }
 

@@ -32,9 +32,9 @@ struct ChunkPtrs {
 template <int NC, int UNROLL>
 __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
                                                               float *__restrict__ out, int prio,
-                                                              uint64_t *stamps) {
+                                                              KTrace tr) {
   set_wave_priority(prio);
-  stamp_begin(stamps);
+  const uint64_t t0 = trace_begin(tr);
   const int nc = NC > 0 ? NC : nchunks;
   const size_t stride = (size_t)gridDim.x * kThreads;
   size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
     }
     __builtin_nontemporal_store(acc, o + i);
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
 // Scalar path: elements [first, len) one at a time (the tail after the vector
@@ -90,16 +90,16 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
 __global__ __launch_bounds__(kThreads) void reduce_scalar_kernel(ChunkPtrs cp, int nchunks,
                                                                  size_t first, size_t len,
                                                                  float *__restrict__ out, int prio,
-                                                                 uint64_t *stamps) {
+                                                                 KTrace tr) {
   set_wave_priority(prio);
-  stamp_begin(stamps);
+  const uint64_t t0 = trace_begin(tr);
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (size_t j = first + (size_t)blockIdx.x * kThreads + threadIdx.x; j < len; j += stride) {
     float acc = cp.p[0][j];
     for (int c = 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
     out[j] = acc;
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
 struct PermTable {
@@ -113,9 +113,9 @@ template <int UNROLL>
 __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
                                                                u32x4 *__restrict__ dst, PermTable pt,
                                                                int nchunks, size_t cvec, int parts,
-                                                               int prio, uint64_t *stamps) {
+                                                               int prio, KTrace tr) {
   set_wave_priority(prio);
-  stamp_begin(stamps);
+  const uint64_t t0 = trace_begin(tr);
   const int nwork = nchunks * parts;
   for (int w = blockIdx.x; w < nwork; w += gridDim.x) {
     const int chunk = w / parts;
@@ -134,7 +134,7 @@ __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__re
     }
     for (; i < hi; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
 // Byte path for unaligned buffers or chunk sizes.
@@ -142,24 +142,25 @@ __global__ __launch_bounds__(kThreads) void permute_byte_kernel(const uint8_t *_
                                                                 uint8_t *__restrict__ dst,
                                                                 PermTable pt, int nchunks,
                                                                 size_t chunk_bytes, int prio,
-                                                                uint64_t *stamps) {
+                                                                KTrace tr) {
   set_wave_priority(prio);
-  stamp_begin(stamps);
+  const uint64_t t0 = trace_begin(tr);
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (int c = 0; c < nchunks; ++c) {
     const uint8_t *s = src + (size_t)pt.p[c] * chunk_bytes;
     uint8_t *d = dst + (size_t)c * chunk_bytes;
     for (size_t b = (size_t)blockIdx.x * kThreads + threadIdx.x; b < chunk_bytes; b += stride) d[b] = s[b];
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
-__global__ void stamps_reset_kernel(uint64_t *stamps, int npairs) {
+__global__ void stamps_reset_kernel(uint64_t *stamps, int npairs, uint32_t *wg) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < npairs) {
+  if (stamps != nullptr && i < npairs) {
     stamps[2 * i] = ~0ull;
     stamps[2 * i + 1] = 0ull;
   }
+  if (wg != nullptr && i == 0) wg[0] = 0u;
 }
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -194,20 +195,20 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
     if (nvec > 0) {
       int g = clamp_wgs(nvec, wgs);
       switch (c.nchunks) {
-        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
-        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
-        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
-        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
-        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.stamps); break;
+        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
+        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
+        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
+        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
+        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
       }
     }
     size_t first = nvec * 4;
     if (first < c.len)
       hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kThreads), 0, s, cp, c.nchunks, first,
-                         c.len, c.out, prio, c.stamps);
+                         c.len, c.out, prio, c.trace);
   } else {
     hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs)), dim3(kThreads), 0, s, cp,
-                       c.nchunks, (size_t)0, c.len, c.out, prio, c.stamps);
+                       c.nchunks, (size_t)0, c.len, c.out, prio, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }
@@ -240,19 +241,20 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     int g = (int)(wgs < items ? wgs : items);
     hipLaunchKernelGGL((permute_vec_kernel<4>), dim3(g), dim3(kThreads), 0, s,
                        static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
-                       c.chunk_bytes / 16, parts, c.priority, c.stamps);
+                       c.chunk_bytes / 16, parts, c.priority, c.trace);
   } else {
     int g = clamp_wgs(c.chunk_bytes, wgs);
     hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kThreads), 0, s,
                        static_cast<const uint8_t *>(c.src), static_cast<uint8_t *>(c.dst), pt,
-                       c.nchunks, c.chunk_bytes, c.priority, c.stamps);
+                       c.nchunks, c.chunk_bytes, c.priority, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }
 
-int stamps_reset(uint64_t *stamps, int npairs, hipStream_t s) {
-  if (stamps == nullptr || npairs <= 0) return OCC_OK;
-  hipLaunchKernelGGL(stamps_reset_kernel, dim3((npairs + 255) / 256), dim3(256), 0, s, stamps, npairs);
+int trace_reset(uint64_t *stamps, int npairs, uint32_t *wg, hipStream_t s) {
+  if (stamps == nullptr && wg == nullptr) return OCC_OK;
+  int n = npairs > 1 ? npairs : 1;
+  hipLaunchKernelGGL(stamps_reset_kernel, dim3((n + 255) / 256), dim3(256), 0, s, stamps, npairs, wg);
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }
 

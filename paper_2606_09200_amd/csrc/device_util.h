@@ -9,17 +9,52 @@ namespace occ {
 // GPU constant-rate clock (100 MHz on CDNA: 10 ns per tick).
 __device__ __forceinline__ uint64_t now_ticks() { return __builtin_amdgcn_s_memrealtime(); }
 
-// Kernel timeline: the first workgroup to start lowers stamps[0], the last to
-// finish raises stamps[1].  Vector atomics on a caller-provided buffer.
-__device__ __forceinline__ void stamp_begin(uint64_t *stamps) {
-  if (stamps != nullptr && threadIdx.x == 0)
-    atomicMin(reinterpret_cast<unsigned long long *>(stamps), (unsigned long long)now_ticks());
+// Optional per-launch tracing.  `stamps` is a [first start, last end] pair
+// (atomic min / max over workgroups); `wg` receives one 32-byte record per
+// workgroup: {tag, block, HW_ID, XCC_ID} then {t0 lo, t0 hi, t1 lo, t1 hi},
+// appended at wg[4 + 8*i] with i taken from the counter wg[0] (records past
+// `wg_cap` are dropped).  HW_ID holds the wave's SIMD [5:4], CU [11:8], SH [12]
+// and SE [15:13]; XCC_ID [3:0] is the XCD.  All accesses are vector atomics or
+// vector stores to the caller's buffer.
+struct KTrace {
+  uint64_t *stamps;
+  uint32_t *wg;
+  uint32_t wg_cap;
+  uint32_t tag;
+};
+
+__device__ __forceinline__ uint64_t trace_begin(const KTrace &t) {
+  uint64_t t0 = 0;
+  if (threadIdx.x == 0 && (t.stamps != nullptr || t.wg != nullptr)) {
+    t0 = now_ticks();
+    if (t.stamps != nullptr)
+      atomicMin(reinterpret_cast<unsigned long long *>(t.stamps), (unsigned long long)t0);
+  }
+  return t0;
 }
-__device__ __forceinline__ void stamp_end(uint64_t *stamps) {
-  if (stamps != nullptr) {
-    __syncthreads();
-    if (threadIdx.x == 0)
-      atomicMax(reinterpret_cast<unsigned long long *>(stamps + 1), (unsigned long long)now_ticks());
+
+__device__ __forceinline__ void trace_end(const KTrace &t, uint64_t t0) {
+  if (t.stamps == nullptr && t.wg == nullptr) return;
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  uint64_t t1 = now_ticks();
+  if (t.stamps != nullptr)
+    atomicMax(reinterpret_cast<unsigned long long *>(t.stamps + 1), (unsigned long long)t1);
+  if (t.wg != nullptr) {
+    uint32_t i = atomicAdd(t.wg, 1u);
+    if (i < t.wg_cap) {
+      uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | 4);    // HW_REG_HW_ID, 32 bits
+      uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);  // HW_REG_XCC_ID, 32 bits
+      uint32_t *r = t.wg + 4 + 8 * (size_t)i;
+      r[0] = t.tag;
+      r[1] = blockIdx.x;
+      r[2] = hw;
+      r[3] = xcc;
+      r[4] = (uint32_t)t0;
+      r[5] = (uint32_t)(t0 >> 32);
+      r[6] = (uint32_t)t1;
+      r[7] = (uint32_t)(t1 >> 32);
+    }
   }
 }
 

@@ -51,11 +51,17 @@ struct Tile {
   static_assert(BM % ROWS_PER_PASS == 0 && BN % ROWS_PER_PASS == 0, "uneven load passes");
 };
 
-// Physical 16-byte chunk of logical chunk c in tile row r.
+// Physical 16-byte chunk of logical chunk c in tile row r.  The LDS has 64
+// banks (256 bytes) and serves a 16-byte-per-lane read 16 lanes at a time;
+// an MFMA operand read sends 16 consecutive rows at one logical chunk per
+// pass.  Rows are 16*KCH bytes long, so 256/(16*KCH) consecutive rows share a
+// bank line at different offsets; XOR-ing the chunk index with the row's
+// line number makes all 16 rows of a pass land on distinct banks.  Stores
+// (KCH consecutive lanes per row, whole rows per pass) stay conflict-free.
 template <int KCH>
 __device__ __forceinline__ int swz(int r, int c) {
-  if constexpr (KCH == 8) return c ^ (r & 7);
-  else return c ^ ((r >> 1) & 3);
+  if constexpr (KCH == 8) return c ^ ((r >> 1) & 7);
+  else return c ^ ((r >> 2) & 3);
 }
 
 // XCD-aware order: dispatch hands consecutive workgroups to the 8 XCDs in
@@ -129,9 +135,10 @@ __global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__res
                                                            const uint16_t *__restrict__ B,
                                                            uint16_t *__restrict__ C, int M, int N,
                                                            int K, int tiles_m, int tiles_n,
-                                                           uint64_t *stamps) {
+                                                           int prio, KTrace tr) {
   extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
-  stamp_begin(stamps);
+  set_wave_priority(prio);
+  const uint64_t t0 = trace_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / T::WN;
@@ -218,7 +225,7 @@ __global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__res
       }
     }
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
 // ---------------------------------------------------------------------------
@@ -233,11 +240,12 @@ constexpr int kSkinnyKB = 128;  // k covered by one wave per block (4 MFMAs)
 __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__restrict__ A,
                                                           const uint16_t *__restrict__ B,
                                                           uint16_t *__restrict__ C, int M, int N,
-                                                          int K, uint64_t *stamps) {
+                                                          int K, int prio, KTrace tr) {
   __shared__ f32x4 partial[3][64];
   extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
   (void)pad_lds;
-  stamp_begin(stamps);
+  set_wave_priority(prio);
+  const uint64_t t0 = trace_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane & 15;   // A row / B row (output column) this lane feeds
@@ -308,13 +316,13 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__rest
       }
     }
   }
-  stamp_end(stamps);
+  trace_end(tr, t0);
 }
 
 // ---------------------------------------------------------------------------
 // Variant table.
 typedef void (*TiledFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, int,
-                        uint64_t *);
+                        int, KTrace);
 
 struct Variant {
   int id;
@@ -435,7 +443,7 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
     }
     int tiles_m = ceil_div(c.M, v->bm), tiles_n = ceil_div(c.N, v->bn);
     hipLaunchKernelGGL(v->fn, dim3(p.grid), dim3(v->threads), dyn, s, A, B, C, c.M, c.N, c.K,
-                       tiles_m, tiles_n, c.stamps);
+                       tiles_m, tiles_n, c.priority, c.trace);
   } else {
     static bool attr_set_skinny = false;
     if (!attr_set_skinny) {
@@ -446,7 +454,7 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
       attr_set_skinny = true;
     }
     hipLaunchKernelGGL(gemm_skinny_kernel, dim3(p.grid), dim3(256), (int)c.lds_bytes, s, A, B, C,
-                       c.M, c.N, c.K, c.stamps);
+                       c.M, c.N, c.K, c.priority, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }

@@ -6,6 +6,7 @@
 #include <stdint.h>
 
 #include "../../include/occ.h"
+#include "device_util.h"
 
 namespace occ {
 
@@ -33,7 +34,8 @@ struct GemmCall {
   size_t lds_bytes;
   int grid_cap;         // 0 = one workgroup per tile
   int variant;          // 0 = automatic, else a kernel variant id
-  uint64_t *stamps;     // optional [start, end] pair (atomic min/max), may be null
+  int priority;         // wave priority 0..3 (s_setprio)
+  KTrace trace;         // optional tracing (all null = off)
 };
 int gemm_plan(const GemmCall &c, occ_gemm_plan *plan);
 int gemm_launch(const GemmCall &c, hipStream_t s);
@@ -46,7 +48,7 @@ struct ReduceCall {
   float *out;
   int wgs;                   // 0 = default
   int priority;              // 0..3
-  uint64_t *stamps;
+  KTrace trace;
 };
 int reduce_launch(const ReduceCall &c, hipStream_t s);
 int reduce_default_wgs(const ReduceCall &c);
@@ -59,7 +61,7 @@ struct PermuteCall {
   size_t chunk_bytes;
   int wgs;
   int priority;
-  uint64_t *stamps;
+  KTrace trace;
 };
 int permute_launch(const PermuteCall &c, hipStream_t s);
 int permute_default_wgs(const PermuteCall &c);
@@ -70,7 +72,8 @@ int validate_reduce(const float *const *bufs, int nchunks, size_t len, const flo
 int validate_permute(const void *src, const void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes);
 
-// Timeline helper: sets n [start, end] pairs to [UINT64_MAX, 0].
-int stamps_reset(uint64_t *stamps, int npairs, hipStream_t s);
+// Tracing helper: sets npairs [start, end] pairs to [UINT64_MAX, 0] and the
+// workgroup-record counter wg[0] to 0 (either pointer may be null).
+int trace_reset(uint64_t *stamps, int npairs, uint32_t *wg, hipStream_t s);
 
 }  // namespace occ

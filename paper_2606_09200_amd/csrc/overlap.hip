@@ -70,19 +70,19 @@ struct Launcher {
   PermuteCall p;
   int kind;
 
-  int gemm(hipStream_t s, uint64_t *stamps) {
+  int gemm(hipStream_t s, KTrace t) {
     GemmCall c = g;
-    c.stamps = stamps;
+    c.trace = t;
     return gemm_launch(c, s);
   }
-  int comm(hipStream_t s, uint64_t *stamps) {
+  int comm(hipStream_t s, KTrace t) {
     if (kind == OCC_COMM_REDUCE) {
       ReduceCall c = r;
-      c.stamps = stamps;
+      c.trace = t;
       return reduce_launch(c, s);
     }
     PermuteCall c = p;
-    c.stamps = stamps;
+    c.trace = t;
     return permute_launch(c, s);
   }
 };
@@ -91,8 +91,10 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c == nullptr) return OCC_EINVAL;
   if (c->n_iter < 1 || c->reps < 1 || c->warmup < 0) return OCC_EINVAL;
   if (c->comm_priority < 0 || c->comm_priority > 3 || c->comm_wgs < 0) return OCC_EINVAL;
+  if (c->gemm_priority < 0 || c->gemm_priority > 3) return OCC_EINVAL;
   if (c->gemm_grid < 0 || c->gemm_variant < 0) return OCC_EINVAL;
   if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) != 0) return OCC_EINVAL;
+  if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
   OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K));
   size_t cbytes = (size_t)c->M * c->N * 2;
   // K_g writes C while K_c runs: C must not overlap anything K_c touches,
@@ -134,9 +136,10 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
 
   Launcher L;
   L.kind = c.comm_kind;
-  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant, nullptr};
-  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, nullptr};
-  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, nullptr};
+  const KTrace off{nullptr, nullptr, 0, 0};
+  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant, c.gemm_priority, off};
+  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off};
+  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off};
 
   occ_gemm_plan plan;
   OCC_TRY(gemm_plan(L.g, &plan));
@@ -163,8 +166,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     if (flags & OCC_RUN_SEQ) {
       OCC_HIP(hipEventRecord(ev[0], s0));
       for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, nullptr);
-        if (st == OCC_OK) st = L.comm(s0, nullptr);
+        st = L.gemm(s0, off);
+        if (st == OCC_OK) st = L.comm(s0, off);
       }
       OCC_HIP(hipEventRecord(ev[1], s0));
       OCC_HIP(hipEventSynchronize(ev[1]));
@@ -180,10 +183,10 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
       OCC_HIP(hipEventRecord(ev[2], s0));
       OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
       for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, nullptr);
+        st = L.gemm(s0, off);
         if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
         if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK) st = L.comm(s1, nullptr);
+        if (st == OCC_OK) st = L.comm(s1, off);
       }
       // C_{n-1} waits on G_{n-1}, the last kernel of the compute stream, so
       // the comm stream's end marks the end of the whole schedule.
@@ -200,9 +203,9 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     if (flags & OCC_RUN_ISO) {
       OCC_HIP(hipEventRecord(iso[0], s0));
       for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, nullptr);
+        st = L.gemm(s0, off);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 1], s0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK) st = L.comm(s0, nullptr);
+        if (st == OCC_OK) st = L.comm(s0, off);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 2], s0) != hipSuccess) st = OCC_EHIP;
       }
       OCC_HIP(hipEventSynchronize(iso[2 * n]));
@@ -225,16 +228,21 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   }
 
   // Timeline: one more, untimed, overlapped repetition with every kernel
-  // stamping its first-start / last-end clock.
-  if (c.timeline != nullptr) {
-    OCC_TRY(stamps_reset(c.timeline, 2 * n, s0));
+  // stamping its first-start / last-end clock and, if asked, one record per
+  // workgroup (tag = 2*iteration + 0 for the GEMM, + 1 for the collective).
+  if (c.timeline != nullptr || c.wg_trace != nullptr) {
+    OCC_TRY(trace_reset(c.timeline, 2 * n, c.wg_trace, s0));
     OCC_HIP(hipEventRecord(ev[2], s0));
     OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
     for (int i = 0; i < n && st == OCC_OK; ++i) {
-      st = L.gemm(s0, c.timeline + 4 * i);
+      KTrace tg{c.timeline ? c.timeline + 4 * i : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
+                (uint32_t)(2 * i)};
+      KTrace tc{c.timeline ? c.timeline + 4 * i + 2 : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
+                (uint32_t)(2 * i + 1)};
+      st = L.gemm(s0, tg);
       if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
       if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
-      if (st == OCC_OK) st = L.comm(s1, c.timeline + 4 * i + 2);
+      if (st == OCC_OK) st = L.comm(s1, tc);
     }
     OCC_HIP(hipEventRecord(ev[3], s1));
     OCC_HIP(hipEventSynchronize(ev[3]));
