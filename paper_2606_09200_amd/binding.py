@@ -24,6 +24,10 @@ GEMM_VARIANTS = {
     0: "auto", 1: "256x256x64 4w", 2: "256x256x64 8w", 3: "256x128x64 4w",
     4: "256x128x64 4w 1-stage", 5: "128x128x64 4w", 6: "opt1 64x64x32", 7: "opt2 64x64x64",
     8: "skinny M<=16", 9: "256x256x32 4w 1-stage",
+    10: "dl 256x256x64 8w 2st", 11: "dl 256x256x32 8w 4st", 12: "dl 256x256x32 8w 3st",
+    13: "dl 256x128x64 4w 3st", 14: "dl 128x128x64 4w 3st", 15: "dl 256x128x64 8w 3st",
+    16: "dl+pipe 256x256x64 8w 2st", 17: "dl+pipe 256x256x32 8w 4st",
+    18: "dl+pipe 256x128x64 4w 3st", 19: "dl+pipe 256x256x64 4w 2st",
 }
 
 

@@ -10,7 +10,7 @@ from gpu_common import DEV, assert_gemm_close, bf16_bits, sample_tiles
 
 pytestmark = pytest.mark.gpu
 
-TILED = [1, 2, 3, 4, 5, 6, 7, 9]
+TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19]
 
 
 def run_gemm(A, B, lds_bytes=0, variant=0, grid_cap=0):
@@ -75,7 +75,7 @@ def test_gemm_tiled_variants_agree_bitwise():
         assert np.array_equal(run_gemm(A, B, variant=v), base), v
 
 
-@pytest.mark.parametrize("variant", [0, 1, 5, 7, 8])
+@pytest.mark.parametrize("variant", [0, 1, 5, 7, 8, 10, 16, 17])
 def test_gemm_pad_and_grid_cap_do_not_change_result(variant):
     M = 16 if variant == 8 else 520
     A, B = inputs.gemm_operands(M, 384, 256, seed=5)
