@@ -1,0 +1,154 @@
+"""Measure every workload configuration and the pad x priority sweep.
+
+    python3 paper_2606_09200_amd/sweep.py --out results.md [--json results.jsonl]
+
+For each point: sequential and overlapped makespans of 10 GEMM -> collective
+iterations (Section 3.2; 5 timed repetitions after 2 warm-up, Section 4.1),
+the reduction 100*(1 - TimeRatio) (Section 4.2), the isolated kernel times
+with the GEMM's MFMA fraction and the comm kernel's HBM fraction, the GEMM's
+resident workgroups per CU (Section 3.1), the overlap rate (Section 4.2) and
+the fraction of comm workgroups that shared a CU with a running GEMM
+workgroup (from the per-workgroup trace).
+"""
+import argparse
+import json
+import os
+import sys
+
+sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+from paper_2606_09200_amd import binding as occ  # noqa: E402
+from paper_2606_09200_amd import inputs  # noqa: E402
+from paper_2606_09200_amd.workloads import WORKLOADS  # noqa: E402
+
+PEAK_TFLOPS = 2500.0
+PEAK_GBS = 8000.0
+
+
+def overlap_rate(tl, n):
+    t = tl.cpu().tolist()
+    g = [(t[4 * i], t[4 * i + 1]) for i in range(n)]
+    c = [(t[4 * i + 2], t[4 * i + 3]) for i in range(n)]
+    tot = sum(e - s for s, e in c)
+    both = sum(max(0, min(ce, ge) - max(cs, gs)) for cs, ce in c for gs, ge in g)
+    return both / tot if tot else 0.0
+
+
+def coresidency(wt):
+    """Fraction of comm workgroups that ran on a CU while a GEMM workgroup did."""
+    recs = occ.decode_wg_trace(wt)
+    if not recs:
+        return None
+    a = np.array([[r["tag"] & 1, r["xcc"] * 64 + r["se"] * 16 + r["sh"] * 8 + r["cu"], r["t0"], r["t1"]]
+                  for r in recs], dtype=np.int64)
+    g = a[a[:, 0] == 0]
+    c = a[a[:, 0] == 1]
+    if len(c) == 0:
+        return None
+    hit = 0
+    for cu, s, e in c[:, 1:]:
+        m = (g[:, 1] == cu) & (g[:, 2] < e) & (g[:, 3] > s)
+        hit += bool(m.any())
+    return hit / len(c)
+
+
+def setup(w, dev):
+    A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_a=w.std_a, std_b=w.std_b,
+                                seed_b=w.seed_b, device=dev)
+    C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
+    if w.comm == "reduce":
+        comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),
+                    out=torch.empty(w.length, device=dev))
+    else:
+        src = inputs.permute_payload(w.nchunks, w.chunk_bytes, seed=2, device=dev)
+        comm = dict(src=src, dst=torch.empty_like(src),
+                    perm=inputs.chunk_permutation(w.nchunks, seed=3), chunk_bytes=w.chunk_bytes)
+    return A, B, C, comm
+
+
+def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0),
+                                   knobs.get("gemm_grid", 0))
+    row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
+           "gemm_variant": plan["kernel_id"], "gemm_tile_lds": plan["tile_lds_bytes"],
+           "gemm_wg_per_cu": plan["wg_per_cu"] if plan["feasible"] else 0, "feasible": plan["feasible"]}
+    if not plan["feasible"]:
+        return row
+    tl = torch.zeros(4 * w.n_iter, dtype=torch.int64, device=dev)
+    wt = torch.zeros(4 + 8 * 60000, dtype=torch.int32, device=dev)
+    r = occ.run_overlap(A, B, C, lds_bytes=pad, comm_priority=prio, n_iter=w.n_iter, reps=reps,
+                        warmup=warmup, timeline=tl, wg_trace=wt, **knobs, **comm)
+    tg, tc = r["t_gemm_ms"], r["t_comm_ms"]
+    row.update({
+        "t_seq_ms": round(r["t_seq_ms"], 4), "t_ovl_ms": round(r["t_ovl_ms"], 4),
+        "reduction_pct": round(r["reduction_pct"], 2),
+        "time_ratio": round(r["t_ovl_ms"] / r["t_seq_ms"], 4),
+        "ideal_ovl_ms": round(w.n_iter * max(tg, tc) + min(tg, tc), 4),
+        "t_gemm_ms": round(tg, 4), "t_comm_ms": round(tc, 4),
+        "gemm_tflops": round(w.gemm_flops / tg / 1e9, 1),
+        "gemm_mfma_frac": round(w.gemm_flops / tg / 1e9 / PEAK_TFLOPS, 4),
+        "gemm_hbm_frac": round(w.gemm_bytes / tg / 1e6 / PEAK_GBS, 4),
+        "comm_gbs": round(w.comm_bytes / tc / 1e6, 1),
+        "comm_hbm_frac": round(w.comm_bytes / tc / 1e6 / PEAK_GBS, 4),
+        "comm_wgs": r["comm_wgs"],
+        "overlap_rate": round(overlap_rate(tl, w.n_iter), 4),
+        "comm_coresident": coresidency(wt),
+    })
+    return row
+
+
+def table(rows):
+    cols = ["workload", "gemm_variant", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
+            "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
+            "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident"]
+    out = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
+    for r in rows:
+        out.append("| " + " | ".join("" if r.get(c) is None else
+                                     ("%.3f" % r[c] if isinstance(r.get(c), float) and c == "comm_coresident" else str(r.get(c, "")))
+                                     for c in cols) + " |")
+    return "\n".join(out)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=None, help="markdown table to write")
+    ap.add_argument("--json", default=None, help="JSON lines to write")
+    ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep")
+    a = ap.parse_args(argv)
+    dev = "cuda:0"
+    rows = []
+    for name in a.workloads.split(","):
+        w = WORKLOADS[name]
+        A, B, C, comm = setup(w, dev)
+        # The pad sweep runs with the default tile (128 KiB of LDS: only small
+        # pads fit) and with tiles small enough for the pad to set residency:
+        # 128x128x64 (96 KiB, three stages) and the paper's opt2 64x64x64.
+        variants = (0, 14, 7) if name == "sweep" else (0,)
+        for variant in variants:
+            base = {}
+            for pad in w.pads:
+                for prio in w.priorities:
+                    row = measure(w, A, B, C, comm, pad, prio, dev, gemm_variant=variant)
+                    if prio == 0:
+                        base[pad] = row.get("t_ovl_ms")
+                    elif base.get(pad) and row.get("t_ovl_ms"):
+                        row["norm_time"] = round(row["t_ovl_ms"] / base[pad], 4)
+                    rows.append(row)
+                    print(json.dumps(row), flush=True)
+        del A, B, C, comm
+        torch.cuda.empty_cache()
+    if a.json:
+        with open(a.json, "w") as f:
+            for r in rows:
+                f.write(json.dumps(r) + "\n")
+    if a.out:
+        with open(a.out, "w") as f:
+            f.write(table(rows) + "\n")
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
