@@ -76,8 +76,25 @@ enum {
   OCC_GEMM_128x128x64_4W = 5,
   OCC_GEMM_OPT1_64x64x32 = 6,
   OCC_GEMM_OPT2_64x64x64 = 7,
-  OCC_GEMM_SKINNY_M16 = 8,   /* M <= 16 only */
-  OCC_GEMM_256x256x32_4W_1STAGE = 9
+  OCC_GEMM_SKINNY_M16 = 8,   /* M <= 16 only (4 waves, 16 k-blocks in flight) */
+  OCC_GEMM_256x256x32_4W_1STAGE = 9,
+  /* direct global->LDS variants (buffer_load ... lds, no staging registers) */
+  OCC_GEMM_DL_256x256x64_8W_2ST = 10,
+  OCC_GEMM_DL_256x256x32_8W_4ST = 11,
+  OCC_GEMM_DL_256x256x32_8W_3ST = 12,
+  OCC_GEMM_DL_256x128x64_4W_3ST = 13,
+  OCC_GEMM_DL_128x128x64_4W_3ST = 14,
+  OCC_GEMM_DL_256x128x64_8W_3ST = 15,
+  /* direct-to-LDS with LDS-read / MFMA interleaving (16: default for large shapes) */
+  OCC_GEMM_DLP_256x256x64_8W_2ST = 16,
+  OCC_GEMM_DLP_256x256x32_8W_4ST = 17,
+  OCC_GEMM_DLP_256x128x64_4W_3ST = 18,
+  OCC_GEMM_DLP_256x256x64_4W_2ST = 19,
+  /* more skinny (M <= 16) variants: waves per workgroup, k-blocks in flight */
+  OCC_GEMM_SKINNY_8W_U16 = 20,
+  OCC_GEMM_SKINNY_8W_U8 = 21,
+  OCC_GEMM_SKINNY_4W_U8 = 22,
+  OCC_GEMM_SKINNY_16W_U8 = 23
 };
 
 /*
@@ -85,11 +102,11 @@ enum {
  * grid_cap > 0 launches at most grid_cap workgroups, each looping over output
  * tiles (persistent workgroups): the "thread-block count" knob of the paper's
  * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
- * and the pad never change the result.  The tiled variants (all but 8)
+ * and the pad never change the result.  The tiled variants (1-7, 9-19)
  * accumulate every output over k in the same order and give bit-identical
- * results; the skinny variant splits K four ways and may differ from them in
- * the last bit.  OCC_EINVAL for an unknown variant or the skinny variant
- * with M > 16.
+ * results; the skinny variants (8, 20-23) split K across waves and may differ
+ * from them, and from each other, in the last bit.  OCC_EINVAL for an unknown
+ * variant or a skinny variant with M > 16.
  */
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);

@@ -432,19 +432,25 @@ __global__ __launch_bounds__(T::NT) void gemm_dl_kernel(const uint16_t *__restri
 }
 
 // ---------------------------------------------------------------------------
-// Skinny kernel for M <= 16 (decode-like GEMMs, HBM-bound on B).  A workgroup
-// owns 16 output columns; its 4 waves split K into contiguous quarters and
-// each streams its share of 16 rows of B straight from HBM into 16x16x32
-// MFMA operands (no LDS staging: every B element is used exactly once).
-// The four partial 16x16 sums are added in wave order 0+1+2+3 through LDS,
-// so the result does not depend on timing.
-constexpr int kSkinnyKB = 128;  // k covered by one wave per block (4 MFMAs)
+// Skinny kernel for M <= 16 (decode-like GEMMs, HBM-bound on B).  Work unit:
+// 16 output columns (16 rows of B) over the whole K.  Persistent workgroups
+// (one per CU by default) loop over units; the 4 waves of a workgroup split
+// K in quarters and stream their share of the 16 B rows straight from HBM
+// into 16x16x32 MFMA operands (non-temporal: every B element is used once),
+// UNROLL 32-wide k-blocks of loads in flight per lane.  In a 32-wide k-block
+// lane l feeds row l % 16 and k-group l / 16, so one load instruction reads a
+// contiguous 64-byte run of each of 16 rows.  A (16 x K, L2-resident) is read
+// the same way.  The four partial 16x16 sums are added in wave order
+// 0+1+2+3 through LDS, so the result does not depend on timing.
+constexpr int kSkinnyKB = 32;
 
-__global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__restrict__ A,
-                                                          const uint16_t *__restrict__ B,
-                                                          uint16_t *__restrict__ C, int M, int N,
-                                                          int K, int prio, KTrace tr) {
-  __shared__ f32x4 partial[3][64];
+template <int WAVES, int UNROLL>
+__global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(const uint16_t *__restrict__ A,
+                                                                 const uint16_t *__restrict__ B,
+                                                                 uint16_t *__restrict__ C, int M,
+                                                                 int N, int K, int prio, KTrace tr) {
+  constexpr int kSkinnyUnroll = UNROLL;  // 32-wide k-blocks in flight per lane
+  __shared__ f32x4 partial[WAVES - 1][64];
   extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
   (void)pad_lds;
   set_wave_priority(prio);
@@ -452,41 +458,42 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__rest
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane & 15;   // A row / B row (output column) this lane feeds
-  const int g = lane >> 4;   // k group
-  const int n0 = blockIdx.x * 16;
+  const int g = lane >> 4;   // 8-wide k group inside a 32-wide k-block
   const int nblk = (K + kSkinnyKB - 1) / kSkinnyKB;
-  const int b0 = wave * nblk / 4, b1 = (wave + 1) * nblk / 4;
+  const int b0 = wave * nblk / WAVES, b1 = (wave + 1) * nblk / WAVES;
   const bool arow_ok = r < M;
-  const bool brow_ok = n0 + r < N;
   const uint16_t *arow = A + (size_t)(arow_ok ? r : 0) * K;
-  const uint16_t *brow = B + (size_t)(brow_ok ? n0 + r : 0) * K;
+  const int units = (N + 15) / 16;
 
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  int b = b0;
-  for (; b + 1 < b1; b += 2) {
-    u32x4 av[8], bv[8];
+  for (int unit = blockIdx.x; unit < units; unit += gridDim.x) {
+    const int n0 = unit * 16;
+    const bool brow_ok = n0 + r < N;
+    const uint16_t *brow = B + (size_t)(brow_ok ? n0 + r : 0) * K;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    int b = b0;
+    for (; b + kSkinnyUnroll <= b1; b += kSkinnyUnroll) {
+      u32x4 av[kSkinnyUnroll], bv[kSkinnyUnroll];
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        int k = (b + u) * kSkinnyKB + g * 32 + s * 8;
-        u32x4 za = {0u, 0u, 0u, 0u}, zb = {0u, 0u, 0u, 0u};
-        if (k < K) {
-          if (arow_ok) za = *reinterpret_cast<const u32x4 *>(arow + k);
-          if (brow_ok) zb = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(brow + k));
-        }
-        av[u * 4 + s] = za;
-        bv[u * 4 + s] = zb;
+      for (int u = 0; u < kSkinnyUnroll; ++u) {
+        const int k = (b + u) * kSkinnyKB + g * 8;
+        u32x4 zb = {0u, 0u, 0u, 0u};
+        if (brow_ok && k < K) zb = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(brow + k));
+        bv[u] = zb;
       }
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[q]),
-                                                    __builtin_bit_cast(bf16x8, bv[q]), acc, 0, 0, 0);
-  }
-  for (; b < b1; ++b) {
+      for (int u = 0; u < kSkinnyUnroll; ++u) {
+        const int k = (b + u) * kSkinnyKB + g * 8;
+        u32x4 za = {0u, 0u, 0u, 0u};
+        if (arow_ok && k < K) za = *reinterpret_cast<const u32x4 *>(arow + k);
+        av[u] = za;
+      }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      int k = b * kSkinnyKB + g * 32 + s * 8;
+      for (int u = 0; u < kSkinnyUnroll; ++u)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av[u]),
+                                                      __builtin_bit_cast(bf16x8, bv[u]), acc, 0, 0, 0);
+    }
+    for (; b < b1; ++b) {
+      const int k = b * kSkinnyKB + g * 8;
       u32x4 za = {0u, 0u, 0u, 0u}, zb = {0u, 0u, 0u, 0u};
       if (k < K) {
         if (arow_ok) za = *reinterpret_cast<const u32x4 *>(arow + k);
@@ -495,29 +502,30 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__rest
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, za),
                                                     __builtin_bit_cast(bf16x8, zb), acc, 0, 0, 0);
     }
-  }
 
-  if (wave > 0) partial[wave - 1][lane] = acc;
-  __syncthreads();
-  if (wave == 0) {
-    f32x4 s = acc;
+    if (wave > 0) partial[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+      f32x4 s = acc;
 #pragma unroll
-    for (int w = 0; w < 3; ++w) {
-      f32x4 p = partial[w][lane];
-      s[0] = s[0] + p[0];
-      s[1] = s[1] + p[1];
-      s[2] = s[2] + p[2];
-      s[3] = s[3] + p[3];
-    }
-    // 16x16 MFMA result layout: lane holds column (lane % 16), rows 4*(lane/16) + i.
-    const int n = n0 + r;
-    if (n < N) {
+      for (int w = 0; w < WAVES - 1; ++w) {
+        f32x4 p = partial[w][lane];
+        s[0] = s[0] + p[0];
+        s[1] = s[1] + p[1];
+        s[2] = s[2] + p[2];
+        s[3] = s[3] + p[3];
+      }
+      // 16x16 MFMA result layout: lane holds column (lane % 16), rows 4*(lane/16) + i.
+      const int n = n0 + r;
+      if (n < N) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int m = 4 * g + i;
-        if (m < M) C[(size_t)m * N + n] = to_bf16(s[i]);
+        for (int i = 0; i < 4; ++i) {
+          int m = 4 * g + i;
+          if (m < M) C[(size_t)m * N + n] = to_bf16(s[i]);
+        }
       }
     }
+    __syncthreads();  // partial[] is reused by the next unit
   }
   trace_end(tr, t0);
 }
@@ -527,21 +535,30 @@ __global__ __launch_bounds__(256) void gemm_skinny_kernel(const uint16_t *__rest
 typedef void (*TiledFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, int,
                         int, KTrace);
 
+typedef void (*SkinnyFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, KTrace);
+
 struct Variant {
   int id;
   int bm, bn, bk, threads, lds;
-  TiledFn fn;  // null: the skinny kernel
+  TiledFn fn;        // tiled kernels
+  SkinnyFn skinny;   // skinny kernels (M <= 16)
   const char *name;
 };
 
 template <class T>
 constexpr Variant make_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, name};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name};
 }
 
 template <class T>
 constexpr Variant make_dl_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, name};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name};
+}
+
+template <int WAVES, int UNROLL>
+constexpr Variant make_skinny_variant(int id, const char *name) {
+  return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, (WAVES - 1) * 64 * 16, nullptr,
+                 gemm_skinny_kernel<WAVES, UNROLL>, name};
 }
 
 using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
@@ -564,7 +581,6 @@ using P256x128_4w_3s = Tile<256, 128, 64, 2, 2, 3, true>;
 using P256x256_4w_2s = Tile<256, 256, 64, 2, 2, 2, true>;
 
 constexpr int kSkinnyId = 8;
-constexpr int kSkinnyStaticLds = 3 * 64 * 16;
 
 const Variant kVariants[] = {
     make_variant<T256x256_4w>(1, "256x256x64 4w 2st"),
@@ -574,7 +590,7 @@ const Variant kVariants[] = {
     make_variant<T128x128_4w>(5, "128x128x64 4w 2st"),
     make_variant<T64x64_opt1>(6, "64x64x32 opt1"),
     make_variant<T64x64_opt2>(7, "64x64x64 opt2"),
-    Variant{kSkinnyId, 16, 16, kSkinnyKB, 256, kSkinnyStaticLds, nullptr, "skinny M<=16"},
+    make_skinny_variant<4, 16>(kSkinnyId, "skinny M<=16, 4 waves"),
     make_variant<T256x256_k32_1s>(9, "256x256x32 4w 1st"),
     make_dl_variant<D256x256_8w_2s>(10, "dl 256x256x64 8w 2st"),
     make_dl_variant<D256x256k32_8w_4s>(11, "dl 256x256x32 8w 4st"),
@@ -586,7 +602,13 @@ const Variant kVariants[] = {
     make_dl_variant<P256x256k32_8w_4s>(17, "dl+pipe 256x256x32 8w 4st"),
     make_dl_variant<P256x128_4w_3s>(18, "dl+pipe 256x128x64 4w 3st"),
     make_dl_variant<P256x256_4w_2s>(19, "dl+pipe 256x256x64 4w 2st"),
+    make_skinny_variant<8, 16>(20, "skinny M<=16, 8 waves"),
+    make_skinny_variant<8, 8>(21, "skinny M<=16, 8 waves, unroll 8"),
+    make_skinny_variant<4, 8>(22, "skinny M<=16, 4 waves, unroll 8"),
+    make_skinny_variant<16, 8>(23, "skinny M<=16, 16 waves, unroll 8"),
 };
+
+bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
 
 const Variant *find_variant(int id) {
   for (const Variant &v : kVariants)
@@ -598,7 +620,7 @@ int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 int auto_variant(int M, int N, int K, int num_cus) {
   (void)K;
-  if (M <= 16) return kSkinnyId;
+  if (M <= 16) return 21;  // skinny, 8 waves, 8 k-blocks in flight
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
   if (big >= num_cus) return 16;
   long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
@@ -611,15 +633,17 @@ int auto_variant(int M, int N, int K, int num_cus) {
 static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_gemm_plan *p) {
   const Variant *v = find_variant(variant);
   if (v == nullptr) return OCC_EINVAL;
-  if (variant == kSkinnyId && c.M > 16) return OCC_EINVAL;
+  const bool skinny = is_skinny(v);
+  if (skinny && c.M > 16) return OCC_EINVAL;
   p->tile_m = v->bm;
   p->tile_n = v->bn;
   p->tile_k = v->bk;
   p->threads = v->threads;
   p->tile_lds_bytes = v->lds;
-  p->tiles = variant == kSkinnyId ? ceil_div(c.N, 16) : ceil_div(c.M, v->bm) * ceil_div(c.N, v->bn);
+  p->tiles = skinny ? ceil_div(c.N, 16) : ceil_div(c.M, v->bm) * ceil_div(c.N, v->bn);
   p->grid = p->tiles;
-  if (variant != kSkinnyId && c.grid_cap > 0 && c.grid_cap < p->grid) p->grid = c.grid_cap;
+  if (skinny && p->grid > di.num_cus) p->grid = di.num_cus;  // persistent, one per CU
+  if (c.grid_cap > 0 && c.grid_cap < p->grid) p->grid = c.grid_cap;
   p->max_lds_per_wg = di.max_lds_per_wg;
   p->lds_per_cu = di.lds_per_cu;
   p->num_cus = di.num_cus;
@@ -643,8 +667,7 @@ int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
   int dyn = (int)(v->fn ? v->lds + c.lds_bytes : c.lds_bytes);
   int nb = 0;
   hipError_t e = v->fn ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, v->fn, v->threads, dyn)
-                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, gemm_skinny_kernel,
-                                                                      v->threads, dyn);
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, v->skinny, v->threads, dyn);
   if (e != hipSuccess) return OCC_EHIP;
   plan->wg_per_cu = nb;
   return OCC_OK;
@@ -673,15 +696,15 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
     hipLaunchKernelGGL(v->fn, dim3(p.grid), dim3(v->threads), dyn, s, A, B, C, c.M, c.N, c.K,
                        tiles_m, tiles_n, c.priority, c.trace);
   } else {
-    static bool attr_set_skinny = false;
-    if (!attr_set_skinny) {
-      if (hipFuncSetAttribute(reinterpret_cast<const void *>(gemm_skinny_kernel),
+    static bool attr_set_skinny[32] = {};
+    if (!attr_set_skinny[v->id]) {
+      if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->skinny),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                              p.max_lds_per_wg - kSkinnyStaticLds) != hipSuccess)
+                              p.max_lds_per_wg - v->lds) != hipSuccess)
         return OCC_EHIP;
-      attr_set_skinny = true;
+      attr_set_skinny[v->id] = true;
     }
-    hipLaunchKernelGGL(gemm_skinny_kernel, dim3(p.grid), dim3(256), (int)c.lds_bytes, s, A, B, C,
+    hipLaunchKernelGGL(v->skinny, dim3(p.grid), dim3(v->threads), (int)c.lds_bytes, s, A, B, C,
                        c.M, c.N, c.K, c.priority, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;

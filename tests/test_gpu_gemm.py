@@ -11,6 +11,7 @@ from gpu_common import DEV, assert_gemm_close, bf16_bits, sample_tiles
 pytestmark = pytest.mark.gpu
 
 TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19]
+SKINNY = [8, 20, 21, 22, 23]
 
 
 def run_gemm(A, B, lds_bytes=0, variant=0, grid_cap=0):
@@ -40,9 +41,9 @@ def test_gemm_auto_full_parity(M, N, K):
     assert frac < 0.05
 
 
-@pytest.mark.parametrize("variant", TILED + [8])
+@pytest.mark.parametrize("variant", TILED + SKINNY)
 def test_gemm_every_variant_ragged(variant):
-    M = 16 if variant == 8 else 300
+    M = 16 if variant in SKINNY else 300
     N, K = 260, 200
     A, B = inputs.gemm_operands(M, N, K, seed=variant)
     got = run_gemm(A, B, variant=variant)
@@ -50,10 +51,10 @@ def test_gemm_every_variant_ragged(variant):
     assert_gemm_close(got, ref, 1.0, 1.0, K, "variant %d" % variant)
 
 
-@pytest.mark.parametrize("variant", TILED + [8])
+@pytest.mark.parametrize("variant", TILED + SKINNY)
 def test_gemm_integer_operands_bit_exact(variant):
     # sums of products of {-2..2} are exact in fp32 in any order: bit-exact
-    M = 13 if variant == 8 else 197
+    M = 13 if variant in SKINNY else 197
     A, B = int_operands(M, 150, 512, seed=variant)
     got = run_gemm(A, B, variant=variant)
     assert np.array_equal(got, oracle.gemm_bf16(A, B, M, 150, 512))
@@ -75,9 +76,9 @@ def test_gemm_tiled_variants_agree_bitwise():
         assert np.array_equal(run_gemm(A, B, variant=v), base), v
 
 
-@pytest.mark.parametrize("variant", [0, 1, 5, 7, 8, 10, 16, 17])
+@pytest.mark.parametrize("variant", [0, 1, 5, 7, 8, 10, 16, 17, 20, 23])
 def test_gemm_pad_and_grid_cap_do_not_change_result(variant):
-    M = 16 if variant == 8 else 520
+    M = 16 if variant in SKINNY else 520
     A, B = inputs.gemm_operands(M, 384, 256, seed=5)
     base = run_gemm(A, B, variant=variant)
     for pad in (16 << 10, 64 << 10):
@@ -146,8 +147,9 @@ def test_gemm_full_size_skinny_full_parity():
     from paper_2606_09200_amd.workloads import WORKLOADS
     w = WORKLOADS["mb"]
     A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=DEV)
-    C = torch.empty((w.M, w.N), device=DEV, dtype=torch.bfloat16)
-    occ.occ_gemm(A, B, C)
-    torch.cuda.synchronize()
     ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), w.M, w.N, w.K)
-    assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full")
+    for v in [0] + SKINNY:
+        C = torch.full((w.M, w.N), float("nan"), device=DEV, dtype=torch.bfloat16)
+        occ.occ_gemm_ex(A, B, C, variant=v)
+        torch.cuda.synchronize()
+        assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full, variant %d" % v)
