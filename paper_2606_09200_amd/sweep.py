@@ -22,7 +22,7 @@ import torch  # noqa: E402
 
 from paper_2606_09200_amd import binding as occ  # noqa: E402
 from paper_2606_09200_amd import inputs  # noqa: E402
-from paper_2606_09200_amd.workloads import WORKLOADS  # noqa: E402
+from paper_2606_09200_amd.workloads import BLOCK_COUNTS, WORKLOADS  # noqa: E402
 
 PEAK_TFLOPS = 2500.0
 PEAK_GBS = 8000.0
@@ -73,6 +73,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
     plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0),
                                    knobs.get("gemm_grid", 0))
     row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
+           "gemm_grid": plan["grid"],
            "gemm_variant": plan["kernel_id"], "gemm_tile_lds": plan["tile_lds_bytes"],
            "gemm_wg_per_cu": plan["wg_per_cu"] if plan["feasible"] else 0, "feasible": plan["feasible"]}
     if not plan["feasible"]:
@@ -101,7 +102,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
 
 
 def table(rows):
-    cols = ["workload", "gemm_variant", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
+    cols = ["workload", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident"]
     out = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
@@ -116,7 +117,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=None, help="markdown table to write")
     ap.add_argument("--json", default=None, help="JSON lines to write")
-    ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep")
+    ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep,blocks")
     a = ap.parse_args(argv)
     dev = "cuda:0"
     rows = []
@@ -126,12 +127,17 @@ def main(argv=None):
         # The pad sweep runs with the default tile (128 KiB of LDS: only small
         # pads fit) and with tiles small enough for the pad to set residency:
         # 128x128x64 (96 KiB, three stages) and the paper's opt2 64x64x64.
-        variants = (0, 14, 7) if name == "sweep" else (0,)
-        for variant in variants:
+        if name == "blocks":
+            points = [dict(gemm_variant=6, gemm_grid=x * x) for x in BLOCK_COUNTS]
+        elif name == "sweep":
+            points = [dict(gemm_variant=v) for v in (0, 14, 7)]
+        else:
+            points = [dict(gemm_variant=0)]
+        for knobs in points:
             base = {}
             for pad in w.pads:
                 for prio in w.priorities:
-                    row = measure(w, A, B, C, comm, pad, prio, dev, gemm_variant=variant)
+                    row = measure(w, A, B, C, comm, pad, prio, dev, **knobs)
                     if prio == 0:
                         base[pad] = row.get("t_ovl_ms")
                     elif base.get(pad) and row.get("t_ovl_ms"):

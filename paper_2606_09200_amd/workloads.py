@@ -66,4 +66,9 @@ WORKLOADS = {
     "sweep": Workload("sweep", 8192, 8192, 8192, "reduce", 8, length=1 << 25,
                       pads=tuple(p * KIB for p in (0, 16, 32, 64, 96, 128)),
                       priorities=(0, 3)),
+    # the paper's thread-block-count axis (Figs. 2-3): cb with the opt1 tile and
+    # a persistent grid of X*X workgroups
+    "blocks": Workload("blocks", 8192, 8192, 8192, "reduce", 8, length=1 << 25,
+                       priorities=(0, 3)),
 }
+BLOCK_COUNTS = (8, 16, 32, 64, 128)   # X = Y; grid = X*X workgroups
