@@ -248,6 +248,24 @@ typedef struct occ_overlap_result {
  */
 int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
 
+/*
+ * occ_overlap_tune -- adaptive choice of the occupancy and priority knobs, the
+ * runtime policy the paper leaves to future work (Section 6).  Times the
+ * overlapped schedule of *cfg (tune_reps repetitions after one warm-up) for
+ * every candidate in
+ *   comm_priority {0, 3} x comm_wgs {library default, one per CU}
+ *   x gemm_grid {one workgroup per tile, one persistent workgroup per CU}
+ *   x lds_bytes {0, the pad that lowers the GEMM's residency by one
+ *                workgroup per CU (only when it has more than one)},
+ * writes the fastest setting into those fields of *cfg (gemm_variant,
+ * n_iter, buffers and the rest are kept), then runs run_overlap(cfg, res)
+ * with it.  *prefer_sequential is set to 1 when even the best overlapped
+ * makespan is longer than the sequential one (then overlap should be off).
+ * Same validation and errors as run_overlap; host-synchronous.
+ */
+int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
+                     int *prefer_sequential);
+
 /* Static string naming a status code. */
 const char *occ_strerror(int status);
 

@@ -83,6 +83,8 @@ _SIGS = {
     "share_permute_ex": [_P, _P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t,
                          ctypes.c_int, ctypes.c_int, _P],
     "run_overlap": [ctypes.POINTER(occ_overlap_cfg), ctypes.POINTER(occ_overlap_result)],
+    "occ_overlap_tune": [ctypes.POINTER(occ_overlap_cfg), ctypes.c_int,
+                         ctypes.POINTER(occ_overlap_result), ctypes.POINTER(ctypes.c_int)],
     "occ_strerror": [ctypes.c_int],
     "occ_version": [],
 }
@@ -229,18 +231,8 @@ def decode_wg_trace(wg_trace):
     return out
 
 
-def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
-                lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0, comm_priority=3,
-                n_iter=10,
-                reps=20, warmup=10, flags=0, timeline=None, wg_trace=None):
-    """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
-
-    Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
-    ``chunk_bytes`` for the alltoall share.  ``timeline``: optional uint64 GPU
-    tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
-    optional int32 GPU tensor of 4 + 8*cap entries (see occ_overlap_cfg.wg_trace).
-    Returns the occ_overlap_result fields as a dict.
-    """
+def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant, gemm_grid,
+              gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace):
     M, N, K = _gemm_args(A, B, C)
     cfg = occ_overlap_cfg()
     cfg.M, cfg.N, cfg.K = M, N, K
@@ -277,6 +269,38 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
             raise ValueError("wg_trace must be a 32-bit tensor of 4 + 8*cap entries")
         cfg.wg_trace = wg_trace.data_ptr()
         cfg.wg_trace_cap = (wg_trace.numel() - 4) // 8
+    return cfg, keep
+
+
+def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
+                lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0,
+                comm_priority=3, n_iter=10, reps=20, warmup=10, flags=0, timeline=None,
+                wg_trace=None):
+    """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
+
+    Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
+    ``chunk_bytes`` for the alltoall share.  ``timeline``: optional uint64 GPU
+    tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
+    optional int32 GPU tensor of 4 + 8*cap entries (see occ_overlap_cfg.wg_trace).
+    Returns the occ_overlap_result fields as a dict.
+    """
+    cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
+                          gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup,
+                          flags, timeline, wg_trace)
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}
+
+
+def occ_overlap_tune(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
+                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3):
+    """Adaptive knob choice (see occ.h).  Returns (chosen knobs, result dict, prefer_sequential)."""
+    cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, 0, gemm_variant, 0, 0, 0,
+                          0, n_iter, reps, warmup, 0, None, None)
+    res = occ_overlap_result()
+    pref = ctypes.c_int(0)
+    _check(lib().occ_overlap_tune(ctypes.byref(cfg), int(tune_reps), ctypes.byref(res),
+                                  ctypes.byref(pref)), "occ_overlap_tune")
+    knobs = {"comm_priority": cfg.comm_priority, "comm_wgs": cfg.comm_wgs,
+             "gemm_grid": cfg.gemm_grid, "lds_bytes": cfg.lds_bytes}
+    return knobs, {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}, bool(pref.value)

@@ -86,6 +86,8 @@ int current_device_info(const DeviceInfo **out) {
 }
 
 int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res);
+int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
+                      int *prefer_sequential);
 
 }  // namespace occ
 
@@ -146,6 +148,11 @@ int share_permute(const void *src, void *dst, const int32_t *perm, int nchunks, 
 
 int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   return occ::run_overlap_impl(cfg, res);
+}
+
+int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
+                     int *prefer_sequential) {
+  return occ::overlap_tune_impl(cfg, tune_reps, res, prefer_sequential);
 }
 
 const char *occ_strerror(int status) {

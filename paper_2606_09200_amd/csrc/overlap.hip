@@ -267,4 +267,73 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   return OCC_OK;
 }
 
+// Adaptive choice of the occupancy and priority knobs (the runtime policy the
+// paper names as future work, Section 6): time the overlapped schedule for
+// each candidate and keep the fastest.  Candidates: comm wave priority
+// {0, 3} x comm workgroups {library default, one per CU} x GEMM grid {one
+// workgroup per tile, persistent one per CU} x extra LDS pad {0, the pad
+// that lowers the GEMM's residency by one workgroup per CU, when one exists}.
+int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
+                      int *prefer_sequential) {
+  if (cfg == nullptr || res == nullptr || prefer_sequential == nullptr || tune_reps < 1)
+    return OCC_EINVAL;
+  OCC_TRY(validate_cfg(cfg));
+  const DeviceInfo *di = nullptr;
+  OCC_TRY(current_device_info(&di));
+
+  // the pad that takes one resident GEMM workgroup per CU away, if any
+  size_t pads[2] = {0, 0};
+  int npads = 1;
+  {
+    GemmCall g{cfg->A, cfg->B, cfg->C, cfg->M, cfg->N, cfg->K, 0, 0, cfg->gemm_variant,
+               cfg->gemm_priority, KTrace{nullptr, nullptr, 0, 0}};
+    occ_gemm_plan p0;
+    OCC_TRY(gemm_plan(g, &p0));
+    if (p0.wg_per_cu > 1) {
+      size_t target = (size_t)di->lds_per_cu / (size_t)p0.wg_per_cu + 1;  // fits one fewer
+      if (target > (size_t)p0.tile_lds_bytes) {
+        g.lds_bytes = target - (size_t)p0.tile_lds_bytes;
+        occ_gemm_plan p1;
+        if (gemm_plan(g, &p1) == OCC_OK && p1.wg_per_cu == p0.wg_per_cu - 1) pads[npads++] = g.lds_bytes;
+      }
+    }
+  }
+  const int prios[2] = {0, 3};
+  const int wgs[2] = {0, di->num_cus};
+  const int grids[2] = {0, di->num_cus};
+
+  occ_overlap_cfg c = *cfg;
+  c.reps = tune_reps;
+  c.warmup = 1;
+  c.flags = OCC_RUN_OVL;
+  c.timeline = nullptr;
+  c.wg_trace = nullptr;
+  double best = 1e300;
+  occ_overlap_cfg best_cfg = c;
+  for (int a = 0; a < 2; ++a)
+    for (int b = 0; b < 2; ++b)
+      for (int d = 0; d < 2; ++d)
+        for (int e = 0; e < npads; ++e) {
+          c.comm_priority = prios[a];
+          c.comm_wgs = wgs[b];
+          c.gemm_grid = grids[d];
+          c.lds_bytes = pads[e];
+          occ_overlap_result r;
+          int st = run_overlap_impl(&c, &r);
+          if (st == OCC_ELDS) continue;
+          if (st != OCC_OK) return st;
+          if (r.t_ovl_ms < best) {
+            best = r.t_ovl_ms;
+            best_cfg = c;
+          }
+        }
+  cfg->comm_priority = best_cfg.comm_priority;
+  cfg->comm_wgs = best_cfg.comm_wgs;
+  cfg->gemm_grid = best_cfg.gemm_grid;
+  cfg->lds_bytes = best_cfg.lds_bytes;
+  OCC_TRY(run_overlap_impl(cfg, res));
+  *prefer_sequential = (res->t_seq_ms > 0 && res->t_ovl_ms > res->t_seq_ms) ? 1 : 0;
+  return OCC_OK;
+}
+
 }  // namespace occ

@@ -117,7 +117,10 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=None, help="markdown table to write")
     ap.add_argument("--json", default=None, help="JSON lines to write")
-    ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep,blocks")
+    ap.add_argument("--tune", action="store_true",
+                    help="also run occ_overlap_tune per workload and report its choice")
+    ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep,blocks,paper_cb_ar,paper_mb_ar,"
+                                           "paper_cb_a2a,paper_mb_a2a")
     a = ap.parse_args(argv)
     dev = "cuda:0"
     rows = []
@@ -144,6 +147,17 @@ def main(argv=None):
                         row["norm_time"] = round(row["t_ovl_ms"] / base[pad], 4)
                     rows.append(row)
                     print(json.dumps(row), flush=True)
+        if a.tune and name not in ("sweep", "blocks"):
+            knobs, r, prefer_seq = occ.occ_overlap_tune(A, B, C, n_iter=w.n_iter, reps=5, warmup=2,
+                                                        tune_reps=3, **comm)
+            row = {"workload": w.name + " (tuned)", "gemm_variant": "auto", "gemm_grid": knobs["gemm_grid"],
+                   "pad_kib": knobs["lds_bytes"] >> 10, "comm_priority": knobs["comm_priority"],
+                   "comm_wgs": knobs["comm_wgs"], "t_seq_ms": round(r["t_seq_ms"], 4),
+                   "t_ovl_ms": round(r["t_ovl_ms"], 4), "reduction_pct": round(r["reduction_pct"], 2),
+                   "t_gemm_ms": round(r["t_gemm_ms"], 4), "t_comm_ms": round(r["t_comm_ms"], 4),
+                   "gemm_wg_per_cu": r["gemm_wg_per_cu"], "prefer_sequential": prefer_seq}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
         del A, B, C, comm
         torch.cuda.empty_cache()
     if a.json:

@@ -13,7 +13,13 @@ collectives on 4-8 GPUs) become one GPU's local share of each collective:
 * ``a2a``     -- expert-like GEMM 16384 x 14336 x 4096 with a 64 x 4 MiB
                  chunk permutation (the local block of an alltoall);
 * ``sweep``   -- ``cb`` over extra LDS pads {0,16,32,64,96,128} KiB x comm wave
-                 priority {normal, high}.
+                 priority {normal, high};
+* ``blocks``  -- ``cb`` with the paper's opt1 tile and a persistent grid of X*X
+                 workgroups (the thread-block-count axis of Figs. 2-3);
+* ``paper_*`` -- Table 1's own pairs on one GPU: cb (8192^3) and mb
+                 (8192 x 57344 x 8192) GEMMs with an 896 MiB local share: a
+                 4-chunk allreduce share (4 x 224 MiB fp32) or a 4-chunk
+                 alltoall share (4 x 224 MiB).
 """
 from dataclasses import dataclass, field
 
@@ -72,3 +78,16 @@ WORKLOADS = {
                        priorities=(0, 3)),
 }
 BLOCK_COUNTS = (8, 16, 32, 64, 128)   # X = Y; grid = X*X workgroups
+
+# Table 1's workloads: 896 MiB collectives, P = 4 chunks of 224 MiB.
+_SHARE = 224 * MIB
+WORKLOADS.update({
+    "paper_cb_ar": Workload("paper_cb_ar", 8192, 8192, 8192, "reduce", 4, length=_SHARE // 4,
+                            priorities=(0, 3)),
+    "paper_mb_ar": Workload("paper_mb_ar", 8192, 57344, 8192, "reduce", 4, length=_SHARE // 4,
+                            priorities=(0, 3)),
+    "paper_cb_a2a": Workload("paper_cb_a2a", 8192, 8192, 8192, "permute", 4, chunk_bytes=_SHARE,
+                             priorities=(0, 3)),
+    "paper_mb_a2a": Workload("paper_mb_a2a", 8192, 57344, 8192, "permute", 4, chunk_bytes=_SHARE,
+                             priorities=(0, 3)),
+})

@@ -113,3 +113,16 @@ def test_run_overlap_argument_errors(L):
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
     cfg.flags = 64
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+
+
+def test_overlap_tune_argument_errors(L):
+    from paper_2606_09200_amd import binding as b
+    cfg = b.occ_overlap_cfg()
+    res = b.occ_overlap_result()
+    pref = ctypes.c_int(0)
+    assert L.occ_overlap_tune(None, 2, ctypes.byref(res), ctypes.byref(pref)) == -1
+    assert L.occ_overlap_tune(ctypes.byref(cfg), 0, ctypes.byref(res), ctypes.byref(pref)) == -1
+    assert L.occ_overlap_tune(ctypes.byref(cfg), 2, None, ctypes.byref(pref)) == -1
+    assert L.occ_overlap_tune(ctypes.byref(cfg), 2, ctypes.byref(res), None) == -1
+    cfg.n_iter = 0  # invalid schedule: rejected before any device call
+    assert L.occ_overlap_tune(ctypes.byref(cfg), 2, ctypes.byref(res), ctypes.byref(pref)) == -1

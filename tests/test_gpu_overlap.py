@@ -100,3 +100,20 @@ def test_plan_reports_occupancy_shaping():
     r0 = occ.occ_gemm_plan_query(8192, 8192, 8192, 0, 5)
     r1 = occ.occ_gemm_plan_query(8192, 8192, 8192, 96 << 10, 5)
     assert r0["wg_per_cu"] >= r1["wg_per_cu"] >= 1
+
+
+def test_overlap_tune_picks_a_candidate_and_keeps_results():
+    A, B, C, chunks, out = tiny_reduce_setup(M=2048, N=2048, K=4096, nchunks=8, length=1 << 23)
+    knobs, r, prefer_seq = occ.occ_overlap_tune(A, B, C, bufs=chunks, out=out, n_iter=6, reps=3,
+                                                warmup=1, tune_reps=2)
+    torch.cuda.synchronize()
+    assert knobs["comm_priority"] in (0, 3)
+    cus = occ.occ_gemm_plan_query(2048, 2048, 4096)["num_cus"]
+    assert knobs["comm_wgs"] in (0, cus)
+    assert knobs["gemm_grid"] in (0, cus)
+    assert r["t_ovl_ms"] > 0 and r["t_seq_ms"] > 0
+    assert prefer_seq == (r["t_ovl_ms"] > r["t_seq_ms"])
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), 2048, 2048, 4096, rows=(0, 64), cols=(1984, 2048))
+    assert_gemm_close(bf16_bits(C)[0:64, 1984:2048], ref, 1.0, 1.0, 4096, "tuned C")
+    assert np.array_equal(out.cpu().numpy().view(np.uint32),
+                          oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
