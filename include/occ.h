@@ -178,8 +178,12 @@ int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunk
 
 enum { OCC_COMM_REDUCE = 0, OCC_COMM_PERMUTE = 1 };
 
-/* run_overlap flags: which passes to time (default 0 means all three). */
-enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4 };
+/* run_overlap flags: which passes to time (no pass bit set means all three),
+   and OCC_RUN_GRAPH: capture the sequential and the overlapped schedule into
+   a HIP graph each and replay it per repetition, instead of issuing every
+   kernel, event record and stream wait from the host (for schedules whose
+   kernels are as short as the host's issue time). */
+enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4, OCC_RUN_GRAPH = 8 };
 
 typedef struct occ_overlap_cfg {
   /* K_g: as occ_gemm */
@@ -240,6 +244,8 @@ typedef struct occ_overlap_result {
  * run_overlap -- time the sequential and the overlapped schedule of n_iter
  * GEMM -> collective iterations (Section 3.2, Fig. 1), after `warmup`
  * untimed repetitions, averaging `reps` timed ones (Section 4.1).
+ * Both schedules end on the compute stream: the overlapped one forks the comm
+ * stream off it with an event and joins it back after the last collective.
  * Host-synchronous.  Uses two library-owned streams of default priority on
  * the current device (created once, kept for the process); the collective's
  * precedence (Section 3.3) is the comm kernel's wave priority.  All three

@@ -93,7 +93,7 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c->comm_priority < 0 || c->comm_priority > 3 || c->comm_wgs < 0) return OCC_EINVAL;
   if (c->gemm_priority < 0 || c->gemm_priority > 3) return OCC_EINVAL;
   if (c->gemm_grid < 0 || c->gemm_variant < 0) return OCC_EINVAL;
-  if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) != 0) return OCC_EINVAL;
+  if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO | OCC_RUN_GRAPH)) != 0) return OCC_EINVAL;
   if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
   OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K));
   size_t cbytes = (size_t)c->M * c->N * 2;
@@ -126,18 +126,67 @@ int validate_cfg(const occ_overlap_cfg *c) {
 
 }  // namespace
 
+namespace {
+
+// The two schedules, enqueued without timing events (so that they can also be
+// captured into a graph).  OVL forks the comm stream off the compute stream
+// and joins it back, so the compute stream's next operation follows both.
+int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KTrace &off) {
+  for (int i = 0; i < n; ++i) {
+    OCC_TRY(L.gemm(s0, off));
+    OCC_TRY(L.comm(s0, off));
+  }
+  return OCC_OK;
+}
+
+int enqueue_ovl(Launcher &L, hipStream_t s0, hipStream_t s1, hipEvent_t fork, hipEvent_t *deps,
+                hipEvent_t join, int n, const KTrace *tg, const KTrace *tc) {
+  OCC_HIP(hipEventRecord(fork, s0));
+  OCC_HIP(hipStreamWaitEvent(s1, fork, 0));
+  for (int i = 0; i < n; ++i) {
+    OCC_TRY(L.gemm(s0, tg[i]));
+    OCC_HIP(hipEventRecord(deps[i], s0));
+    OCC_HIP(hipStreamWaitEvent(s1, deps[i], 0));
+    OCC_TRY(L.comm(s1, tc[i]));
+  }
+  // C_{n-1} waits on G_{n-1}, the last GEMM, so the comm stream's end is the
+  // end of the schedule; the compute stream waits for it.
+  OCC_HIP(hipEventRecord(join, s1));
+  OCC_HIP(hipStreamWaitEvent(s0, join, 0));
+  return OCC_OK;
+}
+
+struct Graph {
+  hipGraph_t g = nullptr;
+  hipGraphExec_t x = nullptr;
+  ~Graph() {
+    if (x) (void)hipGraphExecDestroy(x);
+    if (g) (void)hipGraphDestroy(g);
+  }
+  int end_capture(hipStream_t s) {
+    if (hipStreamEndCapture(s, &g) != hipSuccess) return OCC_EHIP;
+    if (hipGraphInstantiate(&x, g, nullptr, nullptr, 0) != hipSuccess) return OCC_EHIP;
+    return OCC_OK;
+  }
+};
+
+}  // namespace
+
 int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   if (res == nullptr) return OCC_EINVAL;
   OCC_TRY(validate_cfg(cfg));
   memset(res, 0, sizeof *res);
   const occ_overlap_cfg &c = *cfg;
-  const int flags = c.flags ? c.flags : (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO);
+  const int passes = c.flags & (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO);
+  const int flags = (passes ? passes : (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) | (c.flags & OCC_RUN_GRAPH);
+  const bool graph = (flags & OCC_RUN_GRAPH) != 0;
   const int n = c.n_iter;
 
   Launcher L;
   L.kind = c.comm_kind;
   const KTrace off{nullptr, nullptr, 0, 0};
-  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant, c.gemm_priority, off};
+  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
+                 c.gemm_priority, off};
   L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off};
   L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off};
 
@@ -153,11 +202,33 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   OCC_TRY(stream_pair(&sp));
   hipStream_t s0 = sp->comp, s1 = sp->comm;
 
-  Events timing, deps;
+  Events timing, deps, marks;
   OCC_TRY(timing.make(2 * n + 5, hipEventDefault));
   OCC_TRY(deps.make(n, hipEventDisableTiming));
+  OCC_TRY(marks.make(2, hipEventDisableTiming));  // fork, join
   hipEvent_t *ev = timing.ev.data();
   hipEvent_t *iso = ev + 4;  // 2n+1 boundaries of the isolated pass
+  std::vector<KTrace> offs(n, off);
+
+  // Graph mode: capture each schedule once, replay it per repetition.
+  Graph gseq, govl;
+  if (graph) {
+    if (flags & OCC_RUN_SEQ) {
+      OCC_HIP(hipStreamBeginCapture(s0, hipStreamCaptureModeRelaxed));
+      int st = enqueue_seq(L, s0, n, off);
+      int st2 = gseq.end_capture(s0);
+      OCC_TRY(st);
+      OCC_TRY(st2);
+    }
+    if (flags & OCC_RUN_OVL) {
+      OCC_HIP(hipStreamBeginCapture(s0, hipStreamCaptureModeRelaxed));
+      int st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, offs.data(),
+                           offs.data());
+      int st2 = govl.end_capture(s0);
+      OCC_TRY(st);
+      OCC_TRY(st2);
+    }
+  }
 
   double seq_sum = 0, ovl_sum = 0, seq_min = 1e300, ovl_min = 1e300, g_sum = 0, c_sum = 0;
   int st = OCC_OK;
@@ -165,10 +236,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     const bool timed = rep >= c.warmup;
     if (flags & OCC_RUN_SEQ) {
       OCC_HIP(hipEventRecord(ev[0], s0));
-      for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, off);
-        if (st == OCC_OK) st = L.comm(s0, off);
-      }
+      if (graph) st = hipGraphLaunch(gseq.x, s0) == hipSuccess ? OCC_OK : OCC_EHIP;
+      else st = enqueue_seq(L, s0, n, off);
       OCC_HIP(hipEventRecord(ev[1], s0));
       OCC_HIP(hipEventSynchronize(ev[1]));
       if (st != OCC_OK) break;
@@ -181,16 +250,10 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     }
     if (flags & OCC_RUN_OVL) {
       OCC_HIP(hipEventRecord(ev[2], s0));
-      OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
-      for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, off);
-        if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK) st = L.comm(s1, off);
-      }
-      // C_{n-1} waits on G_{n-1}, the last kernel of the compute stream, so
-      // the comm stream's end marks the end of the whole schedule.
-      OCC_HIP(hipEventRecord(ev[3], s1));
+      if (graph) st = hipGraphLaunch(govl.x, s0) == hipSuccess ? OCC_OK : OCC_EHIP;
+      else st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, offs.data(),
+                            offs.data());
+      OCC_HIP(hipEventRecord(ev[3], s0));
       OCC_HIP(hipEventSynchronize(ev[3]));
       if (st != OCC_OK) break;
       float ms = 0;
@@ -227,24 +290,20 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     return st;
   }
 
-  // Timeline: one more, untimed, overlapped repetition with every kernel
-  // stamping its first-start / last-end clock and, if asked, one record per
-  // workgroup (tag = 2*iteration + 0 for the GEMM, + 1 for the collective).
+  // Timeline: one more, untimed, overlapped repetition (eager) with every
+  // kernel stamping its first-start / last-end clock and, if asked, one record
+  // per workgroup (tag = 2*iteration + 0 for the GEMM, + 1 for the collective).
   if (c.timeline != nullptr || c.wg_trace != nullptr) {
     OCC_TRY(trace_reset(c.timeline, 2 * n, c.wg_trace, s0));
-    OCC_HIP(hipEventRecord(ev[2], s0));
-    OCC_HIP(hipStreamWaitEvent(s1, ev[2], 0));
-    for (int i = 0; i < n && st == OCC_OK; ++i) {
-      KTrace tg{c.timeline ? c.timeline + 4 * i : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
-                (uint32_t)(2 * i)};
-      KTrace tc{c.timeline ? c.timeline + 4 * i + 2 : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
-                (uint32_t)(2 * i + 1)};
-      st = L.gemm(s0, tg);
-      if (st == OCC_OK && hipEventRecord(deps.ev[i], s0) != hipSuccess) st = OCC_EHIP;
-      if (st == OCC_OK && hipStreamWaitEvent(s1, deps.ev[i], 0) != hipSuccess) st = OCC_EHIP;
-      if (st == OCC_OK) st = L.comm(s1, tc);
+    std::vector<KTrace> tg(n), tc(n);
+    for (int i = 0; i < n; ++i) {
+      tg[i] = KTrace{c.timeline ? c.timeline + 4 * i : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
+                     (uint32_t)(2 * i)};
+      tc[i] = KTrace{c.timeline ? c.timeline + 4 * i + 2 : nullptr, c.wg_trace,
+                     (uint32_t)c.wg_trace_cap, (uint32_t)(2 * i + 1)};
     }
-    OCC_HIP(hipEventRecord(ev[3], s1));
+    st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, tg.data(), tc.data());
+    OCC_HIP(hipEventRecord(ev[3], s0));
     OCC_HIP(hipEventSynchronize(ev[3]));
     if (st != OCC_OK) return st;
   }
@@ -305,7 +364,7 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   occ_overlap_cfg c = *cfg;
   c.reps = tune_reps;
   c.warmup = 1;
-  c.flags = OCC_RUN_OVL;
+  c.flags = OCC_RUN_OVL | (cfg->flags & OCC_RUN_GRAPH);
   c.timeline = nullptr;
   c.wg_trace = nullptr;
   double best = 1e300;

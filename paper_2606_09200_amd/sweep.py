@@ -69,7 +69,7 @@ def setup(w, dev):
     return A, B, C, comm
 
 
-def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
+def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs):
     plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0),
                                    knobs.get("gemm_grid", 0))
     row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
@@ -81,7 +81,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
     tl = torch.zeros(4 * w.n_iter, dtype=torch.int64, device=dev)
     wt = torch.zeros(4 + 8 * 60000, dtype=torch.int32, device=dev)
     r = occ.run_overlap(A, B, C, lds_bytes=pad, comm_priority=prio, n_iter=w.n_iter, reps=reps,
-                        warmup=warmup, timeline=tl, wg_trace=wt, **knobs, **comm)
+                        warmup=warmup, timeline=tl, wg_trace=wt, flags=flags, **knobs, **comm)
     tg, tc = r["t_gemm_ms"], r["t_comm_ms"]
     row.update({
         "t_seq_ms": round(r["t_seq_ms"], 4), "t_ovl_ms": round(r["t_ovl_ms"], 4),
@@ -102,7 +102,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, **knobs):
 
 
 def table(rows):
-    cols = ["workload", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
+    cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident"]
     out = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
@@ -117,6 +117,8 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=None, help="markdown table to write")
     ap.add_argument("--json", default=None, help="JSON lines to write")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each schedule from a HIP graph (OCC_RUN_GRAPH)")
     ap.add_argument("--tune", action="store_true",
                     help="also run occ_overlap_tune per workload and report its choice")
     ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep,blocks,paper_cb_ar,paper_mb_ar,"
@@ -140,7 +142,9 @@ def main(argv=None):
             base = {}
             for pad in w.pads:
                 for prio in w.priorities:
-                    row = measure(w, A, B, C, comm, pad, prio, dev, **knobs)
+                    row = measure(w, A, B, C, comm, pad, prio, dev,
+                                  flags=occ.OCC_RUN_GRAPH if a.graph else 0, **knobs)
+                    row["graph"] = bool(a.graph)
                     if prio == 0:
                         base[pad] = row.get("t_ovl_ms")
                     elif base.get(pad) and row.get("t_ovl_ms"):

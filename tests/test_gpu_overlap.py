@@ -117,3 +117,38 @@ def test_overlap_tune_picks_a_candidate_and_keeps_results():
     assert_gemm_close(bf16_bits(C)[0:64, 1984:2048], ref, 1.0, 1.0, 4096, "tuned C")
     assert np.array_equal(out.cpu().numpy().view(np.uint32),
                           oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
+
+
+@pytest.mark.parametrize("kind", ["reduce", "permute"])
+def test_graph_replays_match_eager(kind):
+    """OCC_RUN_GRAPH captures both schedules once and replays them (warmup +
+    reps times per call); outputs must equal the eager results after every
+    call, with eager work (refilling the outputs) between the calls."""
+    A, B = inputs.gemm_operands(768, 640, 512, seed=0, device=DEV)
+    C_ref = torch.empty((768, 640), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm(A, B, C_ref)
+    if kind == "reduce":
+        chunks = inputs.reduce_chunks(4, 1 << 18, seed=1, device=DEV)
+        ref = torch.empty(1 << 18, device=DEV)
+        occ.share_reduce(chunks, ref)
+        comm = dict(bufs=chunks, out=torch.empty_like(ref))
+        outk = "out"
+    else:
+        src = inputs.permute_payload(16, 1 << 14, seed=2, device=DEV)
+        perm = inputs.chunk_permutation(16, seed=3)
+        ref = torch.empty_like(src)
+        occ.share_permute(src, ref, perm, 1 << 14)
+        comm = dict(src=src, dst=torch.empty_like(src), perm=perm, chunk_bytes=1 << 14)
+        outk = "dst"
+    torch.cuda.synchronize()
+    C = torch.empty_like(C_ref)
+    for call in range(3):
+        C.fill_(float("nan"))
+        comm[outk].fill_(7)
+        torch.cuda.synchronize()
+        r = occ.run_overlap(A, B, C, n_iter=3, reps=2, warmup=1 + call,
+                            flags=occ.OCC_RUN_SEQ | occ.OCC_RUN_OVL | occ.OCC_RUN_GRAPH, **comm)
+        torch.cuda.synchronize()
+        assert r["t_seq_ms"] > 0 and r["t_ovl_ms"] > 0
+        assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16)), call
+        assert torch.equal(comm[outk].view(torch.uint8), ref.view(torch.uint8)), call
