@@ -94,7 +94,12 @@ enum {
   OCC_GEMM_SKINNY_8W_U16 = 20,
   OCC_GEMM_SKINNY_8W_U8 = 21,
   OCC_GEMM_SKINNY_4W_U8 = 22,
-  OCC_GEMM_SKINNY_16W_U8 = 23
+  OCC_GEMM_SKINNY_16W_U8 = 23,
+  /* two resident workgroups per CU (independent barriers), 4 waves each */
+  OCC_GEMM_DLP_256x128x32_4W_2ST = 24,
+  OCC_GEMM_DLP_128x256x32_4W_2ST = 25,
+  OCC_GEMM_DLP_256x128x32_4W_3ST = 26,
+  OCC_GEMM_DLP_128x256x32_4W_3ST = 27
 };
 
 /*
@@ -102,7 +107,7 @@ enum {
  * grid_cap > 0 launches at most grid_cap workgroups, each looping over output
  * tiles (persistent workgroups): the "thread-block count" knob of the paper's
  * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
- * and the pad never change the result.  The tiled variants (1-7, 9-19)
+ * and the pad never change the result.  The tiled variants (1-7, 9-19, 24-27)
  * accumulate every output over k in the same order and give bit-identical
  * results; the skinny variants (8, 20-23) split K across waves and may differ
  * from them, and from each other, in the last bit.  OCC_EINVAL for an unknown

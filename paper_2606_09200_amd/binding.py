@@ -29,6 +29,8 @@ GEMM_VARIANTS = {
     16: "dl+pipe 256x256x64 8w 2st", 17: "dl+pipe 256x256x32 8w 4st",
     18: "dl+pipe 256x128x64 4w 3st", 19: "dl+pipe 256x256x64 4w 2st",
     20: "skinny 8w u16", 21: "skinny 8w u8", 22: "skinny 4w u8", 23: "skinny 16w u8",
+    24: "dl+pipe 256x128x32 4w 2st 2wg/cu", 25: "dl+pipe 128x256x32 4w 2st 2wg/cu",
+    26: "dl+pipe 256x128x32 4w 3st 2wg/cu", 27: "dl+pipe 128x256x32 4w 3st 2wg/cu",
 }
 SKINNY_VARIANTS = (8, 20, 21, 22, 23)
 

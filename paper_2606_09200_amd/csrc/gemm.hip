@@ -32,10 +32,11 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 // so that the 32 rows of an MFMA operand read hit distinct banks), with the
 // next k-step's global loads in flight in registers while the current one is
 // multiplied.  STAGES = 2 double-buffers the LDS (one barrier per k-step).
-template <int BM_, int BN_, int BK_, int WM_, int WN_, int STAGES_, bool PIPE_ = false>
+template <int BM_, int BN_, int BK_, int WM_, int WN_, int STAGES_, bool PIPE_ = false, int MINB_ = 1>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_, STAGES = STAGES_;
   static constexpr bool PIPE = PIPE_;  // enforce LDS-read / MFMA interleaving
+  static constexpr int MINB = MINB_;   // workgroups per CU the register budget must allow
   static constexpr int NT = 64 * WM * WN;
   static constexpr int TM = BM / WM, TN = BN / WN;
   static constexpr int FM = TM / 32, FN = TN / 32;
@@ -285,7 +286,7 @@ __device__ __forceinline__ void wait_stages(int ahead) {
 }
 
 template <class T>
-__global__ __launch_bounds__(T::NT) void gemm_dl_kernel(const uint16_t *__restrict__ A,
+__global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t *__restrict__ A,
                                                         const uint16_t *__restrict__ B,
                                                         uint16_t *__restrict__ C, int M, int N,
                                                         int K, int tiles_m, int tiles_n, int prio,
@@ -579,6 +580,12 @@ using P256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true>;
 using P256x256k32_8w_4s = Tile<256, 256, 32, 2, 4, 4, true>;
 using P256x128_4w_3s = Tile<256, 128, 64, 2, 2, 3, true>;
 using P256x256_4w_2s = Tile<256, 256, 64, 2, 2, 2, true>;
+// two workgroups per CU: each has its own barriers, so one computes while the
+// other waits (48-72 KiB of LDS, 4 waves of 128x64 each)
+using P256x128k32_4w_2s = Tile<256, 128, 32, 2, 2, 2, true, 2>;
+using P128x256k32_4w_2s = Tile<128, 256, 32, 1, 4, 2, true, 2>;
+using P256x128k32_4w_3s = Tile<256, 128, 32, 2, 2, 3, true, 2>;
+using P128x256k32_4w_3s = Tile<128, 256, 32, 1, 4, 3, true, 2>;
 
 constexpr int kSkinnyId = 8;
 
@@ -606,6 +613,10 @@ const Variant kVariants[] = {
     make_skinny_variant<8, 8>(21, "skinny M<=16, 8 waves, unroll 8"),
     make_skinny_variant<4, 8>(22, "skinny M<=16, 4 waves, unroll 8"),
     make_skinny_variant<16, 8>(23, "skinny M<=16, 16 waves, unroll 8"),
+    make_dl_variant<P256x128k32_4w_2s>(24, "dl+pipe 256x128x32 4w 2st"),
+    make_dl_variant<P128x256k32_4w_2s>(25, "dl+pipe 128x256x32 4w 2st"),
+    make_dl_variant<P256x128k32_4w_3s>(26, "dl+pipe 256x128x32 4w 3st"),
+    make_dl_variant<P128x256k32_4w_3s>(27, "dl+pipe 128x256x32 4w 3st"),
 };
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }

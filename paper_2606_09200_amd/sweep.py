@@ -131,11 +131,12 @@ def main(argv=None):
         A, B, C, comm = setup(w, dev)
         # The pad sweep runs with the default tile (128 KiB of LDS: only small
         # pads fit) and with tiles small enough for the pad to set residency:
-        # 128x128x64 (96 KiB, three stages) and the paper's opt2 64x64x64.
+        # 128x256x32 (48 KiB, two per CU), 128x128x64 (96 KiB, three stages) and
+        # the paper's opt2 64x64x64.
         if name == "blocks":
             points = [dict(gemm_variant=6, gemm_grid=x * x) for x in BLOCK_COUNTS]
         elif name == "sweep":
-            points = [dict(gemm_variant=v) for v in (0, 14, 7)]
+            points = [dict(gemm_variant=v) for v in (0, 25, 14, 7)]
         else:
             points = [dict(gemm_variant=0)]
         for knobs in points:

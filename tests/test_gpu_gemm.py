@@ -10,7 +10,7 @@ from gpu_common import DEV, assert_gemm_close, bf16_bits, sample_tiles
 
 pytestmark = pytest.mark.gpu
 
-TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19]
+TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 24, 25, 26, 27]
 SKINNY = [8, 20, 21, 22, 23]
 
 
