@@ -296,6 +296,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
   const uint64_t t0 = trace_begin(tr);
   constexpr int S = T::STAGES;
   constexpr int PER_STAGE = T::A_LOADS + T::B_LOADS;
+  static_assert(T::ROWS_PER_PASS % 16 == 0, "a lane's swizzle must not change between passes");
   constexpr int ROW_BYTES = T::BK * 2;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -305,13 +306,15 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
   const int nk = (K + T::BK - 1) / T::BK;
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) unsigned char *)smem;
 
-  // This lane's slot in every load pass: row r_in (+ p*ROWS_PER_PASS),
-  // physical chunk q; the swizzle is the same for all passes of a lane.
+  // This lane's slot in every load pass: row r_in of the pass, physical
+  // chunk q; the swizzle is the same for all passes of a lane, so one offset
+  // (plus k0) serves every pass: each pass gets a buffer descriptor of its
+  // own, based at the pass's first row, whose num_records covers only the
+  // pass's rows that exist.
   const int r_in = threadIdx.x / T::KCH;
   const int q = threadIdx.x % T::KCH;
   const int c = q ^ (swz<T::KCH>(r_in, 0));
   const uint32_t lane_off = (uint32_t)r_in * (uint32_t)K * 2u + (uint32_t)c * 16u;
-  const uint32_t pass_off = (uint32_t)T::ROWS_PER_PASS * (uint32_t)K * 2u;
   const uint32_t wave_lds = (uint32_t)wave * 1024u;
 
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
@@ -319,21 +322,22 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
     tile_coords<8>(xcd_remap(t, ntiles), tiles_m, tiles_n, tm, tn);
     const int m0 = tm * T::BM;
     const int n0 = tn * T::BN;
-    const i32x4 rsa = make_rsrc(A + (size_t)m0 * K, (uint32_t)min(T::BM, M - m0) * (uint32_t)K * 2u);
-    const i32x4 rsb = make_rsrc(B + (size_t)n0 * K, (uint32_t)min(T::BN, N - n0) * (uint32_t)K * 2u);
 
+    auto pass_rsrc = [&](const uint16_t *base, int row0, int rows) {
+      const int have = min(T::ROWS_PER_PASS, max(0, rows - row0));
+      return make_rsrc(base + (size_t)row0 * K, (uint32_t)have * (uint32_t)K * 2u);
+    };
     auto issue = [&](int kt) {
       const int k0 = kt * T::BK;
       const uint32_t sbase = lds0 + (uint32_t)((kt % S) * T::STAGE_BYTES) + wave_lds;
-      const bool kok = k0 + c * 8 < K;
-      const uint32_t v0 = kok ? lane_off + (uint32_t)k0 * 2u : 0x80000000u;
+      const uint32_t v = (k0 + c * 8 < K) ? lane_off + (uint32_t)k0 * 2u : 0x80000000u;
 #pragma unroll
       for (int p = 0; p < T::A_LOADS; ++p)
-        lds_dma16(rsa, sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), kok ? v0 + p * pass_off : v0);
+        lds_dma16(pass_rsrc(A, m0 + p * T::ROWS_PER_PASS, M), sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), v);
 #pragma unroll
       for (int p = 0; p < T::B_LOADS; ++p)
-        lds_dma16(rsb, sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES),
-                  kok ? v0 + p * pass_off : v0);
+        lds_dma16(pass_rsrc(B, n0 + p * T::ROWS_PER_PASS, N),
+                  sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES), v);
     };
 
     f32x16 acc[T::FM][T::FN];
@@ -426,6 +430,9 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
             if (m < M) C[(size_t)m * N + n] = to_bf16(acc[i][j][r]);
           }
         }
+        // keep the accumulator reads of one block next to its stores (the
+        // scheduler would otherwise hoist all of them and exhaust registers)
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
