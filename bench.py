@@ -126,6 +126,8 @@ def main():
     ap.add_argument("--variant", type=int, default=0, help="GEMM kernel variant (0 = auto)")
     ap.add_argument("--gemm-grid", type=int, default=0, help="persistent GEMM grid cap (0 = off)")
     ap.add_argument("--comm-wgs", type=int, default=0)
+    ap.add_argument("--comm-rate-gbs", type=float, default=0.0,
+                    help="bandwidth pacing of the collective in the overlapped schedule (0 = off)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -145,7 +147,8 @@ def main():
     A, B, C, comm = make_inputs(w, dev)
     torch.cuda.synchronize()
     knobs = dict(lds_bytes=args.pad_kib << 10, gemm_variant=args.variant, gemm_grid=args.gemm_grid,
-                 comm_wgs=args.comm_wgs, comm_priority=args.priority, n_iter=w.n_iter)
+                 comm_wgs=args.comm_wgs, comm_priority=args.priority, n_iter=w.n_iter,
+                 comm_rate_gbs=args.comm_rate_gbs)
 
     # untimed warmup steps, then exactly `steps` timed steps
     occ.run_overlap(A, B, C, reps=args.warmup, warmup=0, **knobs, **comm) if args.warmup > 0 else None
@@ -162,19 +165,20 @@ def main():
                            **knobs_lo, **comm)
     torch.cuda.synchronize()
 
-    # kernel timeline of one more overlapped pass (overlap rate, Section 4.2)
+    # kernel timeline and per-workgroup trace of one more overlapped pass:
+    # overlap rate (Section 4.2), co-residency, and the GEMM workgroups'
+    # lifetime and engine clock with and without the collective running
+    from paper_2606_09200_amd import trace
     tl = torch.zeros(4 * w.n_iter, dtype=torch.int64, device=dev)
-    occ.run_overlap(A, B, C, reps=1, warmup=0, flags=occ.OCC_RUN_OVL, timeline=tl, **knobs, **comm)
+    wt = torch.zeros(4 + occ.WG_RECORD_WORDS * 40 * 1024, dtype=torch.int32, device=dev)
+    occ.run_overlap(A, B, C, reps=1, warmup=0, flags=occ.OCC_RUN_OVL, timeline=tl, wg_trace=wt,
+                    **knobs, **comm)
     torch.cuda.synchronize()
-    t = tl.cpu().tolist()
-    g_iv = [(t[4 * i], t[4 * i + 1]) for i in range(w.n_iter)]
-    c_iv = [(t[4 * i + 2], t[4 * i + 3]) for i in range(w.n_iter)]
-    comm_time = sum(e - s for s, e in c_iv)
-    both = 0
-    for cs, ce in c_iv:            # comm intervals are disjoint (one stream), as are GEMM intervals
-        for gs, ge in g_iv:
-            both += max(0, min(ce, ge) - max(cs, gs))
-    overlap_rate = both / comm_time if comm_time > 0 else 0.0
+    g_iv, c_iv = trace.intervals(tl.cpu(), w.n_iter)
+    overlap_rate = trace.overlap_rate(g_iv, c_iv)
+    recs = occ.decode_wg_trace(wt)
+    inter = trace.interference(recs, c_iv)
+    cores = trace.coresidency(recs)
 
     gemm_tflops = w.gemm_flops / (r["t_gemm_ms"] * 1e-3) / 1e12
     comm_gbs = w.comm_bytes / (r["t_comm_ms"] * 1e-3) / 1e9
@@ -221,6 +225,7 @@ def main():
             "gemm_wg_per_cu": plan["wg_per_cu"],
             "gemm_grid": plan["grid"],
             "comm_wgs": r["comm_wgs"],
+            "comm_rate_gbs": args.comm_rate_gbs,
             "parallelism": "single GPU",
         },
         "t_seq_ms": round(r["t_seq_ms"], 4),
@@ -234,6 +239,8 @@ def main():
         "comm_gbs": round(comm_gbs, 1),
         "comm_hbm_frac": round(comm_gbs / PEAK_HBM_GBS, 4),
         "overlap_rate": round(overlap_rate, 4),
+        "comm_coresident": None if cores is None else round(cores, 4),
+        "gemm_wg": inter,
         "t_ovl_normal_priority_ms": round(r_lo["t_ovl_ms"], 4),
         "reduction_pct_normal_priority": round(100.0 * (1.0 - r_lo["t_ovl_ms"] / r["t_seq_ms"]), 3),
         "norm_time_priority": round(r["t_ovl_ms"] / r_lo["t_ovl_ms"], 4),

@@ -221,16 +221,28 @@ typedef struct occ_overlap_cfg {
      10 ns ticks of the GPU's constant-rate clock (earliest workgroup start,
      latest workgroup end).  NULL = no timeline. */
   uint64_t *timeline;
-  /* optional device buffer of 4 + 8*wg_trace_cap uint32: for that same
-     repetition, word 0 counts workgroups and record i (words 4+8i .. 11+8i)
-     is {tag, workgroup id, HW_ID, XCC_ID, t0 lo, t0 hi, t1 lo, t1 hi}: tag =
-     2*iteration (+1 for the collective), HW_ID/XCC_ID the hardware registers
-     naming the CU (bits 11:8), shader array (12), shader engine (15:13) and
-     XCD (3:0), t0/t1 the workgroup's start/end clock (10 ns ticks).  Records
-     beyond wg_trace_cap are counted but not written.  NULL = off. */
+  /* optional device buffer of 4 + 12*wg_trace_cap uint32: for that same
+     repetition, word 0 counts workgroups and record i (words 4+12i ..
+     15+12i) is {tag, workgroup id, HW_ID, XCC_ID, t0 lo, t0 hi, t1 lo, t1 hi,
+     cycles lo, cycles hi, 0, 0}: tag = 2*iteration (+1 for the collective),
+     HW_ID/XCC_ID the hardware registers naming the CU (bits 11:8), shader
+     array (12), shader engine (15:13) and XCD (3:0), t0/t1 the workgroup's
+     start/end clock (10 ns ticks), cycles the engine-clock cycles between
+     them (cycles / (t1 - t0) / 10 ns = the clock the workgroup ran at).
+     Records beyond wg_trace_cap are counted but not written.  NULL = off. */
   uint32_t *wg_trace;
   int wg_trace_cap;
+  /* bandwidth pacing of the collective in the overlapped schedule, GB/s over
+     the whole grid: every comm wave spaces its load/store trips so that the
+     kernel streams at no more than this rate, leaving memory bandwidth to the
+     co-running GEMM.  0 = unpaced (full speed); otherwise at least
+     OCC_MIN_COMM_RATE_GBS.  The sequential schedule and the isolated kernel
+     timings always run unpaced, so t_seq stays the fastest sequential
+     makespan.  Results are unchanged (same arithmetic, same order). */
+  double comm_rate_gbs;
 } occ_overlap_cfg;
+
+#define OCC_MIN_COMM_RATE_GBS 10.0
 
 typedef struct occ_overlap_result {
   double t_seq_ms;        /* mean sequential makespan: one stream, G0 C0 G1 C1 ... */
@@ -256,6 +268,13 @@ typedef struct occ_overlap_result {
  * precedence (Section 3.3) is the comm kernel's wave priority.  All three
  * passes compute the same outputs: C, out/dst are identical to one occ_gemm
  * and one share_* call.  Buffers are validated as by those entry points.
+ * HIP maps a process's streams onto a fixed number of hardware queues
+ * (GPU_MAX_HW_QUEUES, 4 by default), round-robin in creation order; once a
+ * process holds more streams than queues, the two launcher streams can land
+ * on one queue and the "overlapped" schedule then runs serially.  Callers
+ * that create streams of their own should keep the total within the queue
+ * count (measured: 9.9 ms overlapped with 3 streams in the process, 10.7 ms
+ * -- no overlap -- with 5, for the 8192^3 GEMM + 8 x 2^25 fp32 reduce).
  */
 int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
 

@@ -33,6 +33,8 @@ GEMM_VARIANTS = {
     26: "dl+pipe 256x128x32 4w 3st 2wg/cu", 27: "dl+pipe 128x256x32 4w 3st 2wg/cu",
 }
 SKINNY_VARIANTS = (8, 20, 21, 22, 23)
+MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
+WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
 
 class OccError(RuntimeError):
@@ -60,6 +62,7 @@ class occ_overlap_cfg(ctypes.Structure):
         ("n_iter", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
         ("flags", ctypes.c_int), ("timeline", ctypes.c_void_p),
         ("wg_trace", ctypes.c_void_p), ("wg_trace_cap", ctypes.c_int),
+        ("comm_rate_gbs", ctypes.c_double),
     ]
 
 
@@ -221,26 +224,29 @@ def share_permute(src, dst, perm, chunk_bytes, stream=None, wgs=0, priority=0):
 def decode_wg_trace(wg_trace):
     """Records of a filled wg_trace tensor as a list of dicts (host side)."""
     w = wg_trace.cpu().numpy().astype("int64") & 0xFFFFFFFF
-    n = min(int(w[0]), (w.size - 4) // 8)
+    n = min(int(w[0]), (w.size - 4) // WG_RECORD_WORDS)
     out = []
     for i in range(n):
-        r = w[4 + 8 * i: 12 + 8 * i]
+        r = w[4 + WG_RECORD_WORDS * i: 4 + WG_RECORD_WORDS * (i + 1)]
         hw, xcc = int(r[2]), int(r[3])
         out.append({"tag": int(r[0]), "iter": int(r[0]) >> 1, "kind": "comm" if r[0] & 1 else "gemm",
                     "block": int(r[1]), "cu": (hw >> 8) & 0xF, "sh": (hw >> 12) & 1,
                     "se": (hw >> 13) & 0x7, "xcc": xcc & 0xF,
-                    "t0": int(r[4]) | (int(r[5]) << 32), "t1": int(r[6]) | (int(r[7]) << 32)})
+                    "t0": int(r[4]) | (int(r[5]) << 32), "t1": int(r[6]) | (int(r[7]) << 32),
+                    "cycles": int(r[8]) | (int(r[9]) << 32)})
     return out
 
 
 def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant, gemm_grid,
-              gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace):
+              gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace,
+              comm_rate_gbs=0.0):
     M, N, K = _gemm_args(A, B, C)
     cfg = occ_overlap_cfg()
     cfg.M, cfg.N, cfg.K = M, N, K
     cfg.A, cfg.B, cfg.C = _ptr(A).value, _ptr(B).value, _ptr(C).value
     cfg.lds_bytes, cfg.gemm_variant, cfg.gemm_grid = int(lds_bytes), int(gemm_variant), int(gemm_grid)
     cfg.gemm_priority = int(gemm_priority)
+    cfg.comm_rate_gbs = float(comm_rate_gbs)
     keep = []
     if bufs is not None:
         arr, n, length = _chunk_ptrs(bufs)
@@ -267,28 +273,29 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
             raise ValueError("timeline must hold 4*n_iter 64-bit entries")
         cfg.timeline = timeline.data_ptr()
     if wg_trace is not None:
-        if wg_trace.dtype not in (torch.int32, torch.uint32) or wg_trace.numel() < 12:
-            raise ValueError("wg_trace must be a 32-bit tensor of 4 + 8*cap entries")
+        if wg_trace.dtype not in (torch.int32, torch.uint32) or wg_trace.numel() < 4 + WG_RECORD_WORDS:
+            raise ValueError("wg_trace must be a 32-bit tensor of 4 + %d*cap entries" % WG_RECORD_WORDS)
         cfg.wg_trace = wg_trace.data_ptr()
-        cfg.wg_trace_cap = (wg_trace.numel() - 4) // 8
+        cfg.wg_trace_cap = (wg_trace.numel() - 4) // WG_RECORD_WORDS
     return cfg, keep
 
 
 def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
                 lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0,
                 comm_priority=3, n_iter=10, reps=20, warmup=10, flags=0, timeline=None,
-                wg_trace=None):
+                wg_trace=None, comm_rate_gbs=0.0):
     """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
 
     Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
     ``chunk_bytes`` for the alltoall share.  ``timeline``: optional uint64 GPU
     tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
-    optional int32 GPU tensor of 4 + 8*cap entries (see occ_overlap_cfg.wg_trace).
-    Returns the occ_overlap_result fields as a dict.
+    optional int32 GPU tensor of 4 + 12*cap entries (see occ_overlap_cfg.wg_trace).
+    ``comm_rate_gbs``: bandwidth pacing of the collective in the overlapped
+    schedule (0 = full speed).  Returns the occ_overlap_result fields as a dict.
     """
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
                           gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup,
-                          flags, timeline, wg_trace)
+                          flags, timeline, wg_trace, comm_rate_gbs)
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}

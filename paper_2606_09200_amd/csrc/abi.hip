@@ -122,7 +122,7 @@ int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *ou
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (len > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}};
+  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0};
   return occ::reduce_launch(c, static_cast<hipStream_t>(stream));
 }
 
@@ -137,7 +137,7 @@ int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunk
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (chunk_bytes > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}};
+  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0};
   return occ::permute_launch(c, static_cast<hipStream_t>(stream));
 }
 

@@ -35,16 +35,18 @@ struct ChunkPtrs {
 template <int NC, int UNROLL>
 __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
                                                               float *__restrict__ out, int prio,
-                                                              KTrace tr) {
+                                                              uint32_t pace, KTrace tr) {
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
+  Pacer pc = pace_start(pace);
   const int nc = NC > 0 ? NC : nchunks;
   const size_t stride = (size_t)gridDim.x * kThreads;
   size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
   f32x4 *o = reinterpret_cast<f32x4 *>(out);
 
   if constexpr (NC > 0) {
-    for (; i + (UNROLL - 1) * stride < nvec; i += UNROLL * stride) {
+    for (bool first = true; i + (UNROLL - 1) * stride < nvec; i += UNROLL * stride, first = false) {
+      if (!first) pace_wait(pc);
       f32x4 v[NC][UNROLL];
 #pragma unroll
       for (int c = 0; c < NC; ++c)
@@ -67,7 +69,8 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
   }
   // Remaining positions (and every position when the chunk count is only
   // known at run time): chunks in batches of 8 loads, folded in order.
-  for (; i < nvec; i += stride) {
+  for (bool first = true; i < nvec; i += stride, first = false) {
+    if (NC == 0 && !first) pace_wait(pc);
     f32x4 acc = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[0]) + i);
     for (int c0 = 1; c0 < nc; c0 += 8) {
       f32x4 v[8];
@@ -95,7 +98,7 @@ __global__ __launch_bounds__(kThreads) void reduce_scalar_kernel(ChunkPtrs cp, i
                                                                  float *__restrict__ out, int prio,
                                                                  KTrace tr) {
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (size_t j = first + (size_t)blockIdx.x * kThreads + threadIdx.x; j < len; j += stride) {
     float acc = cp.p[0][j];
@@ -116,9 +119,11 @@ template <int UNROLL>
 __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
                                                                u32x4 *__restrict__ dst, PermTable pt,
                                                                int nchunks, size_t cvec, int parts,
-                                                               int prio, KTrace tr) {
+                                                               int prio, uint32_t pace, KTrace tr) {
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
+  Pacer pc = pace_start(pace);
+  bool first = true;
   const int nwork = nchunks * parts;
   for (int w = blockIdx.x; w < nwork; w += gridDim.x) {
     const int chunk = w / parts;
@@ -129,6 +134,8 @@ __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__re
     u32x4 *d = dst + (size_t)chunk * cvec;
     size_t i = lo + threadIdx.x;
     for (; i + (UNROLL - 1) * kThreads < hi; i += UNROLL * kThreads) {
+      if (!first) pace_wait(pc);
+      first = false;
       u32x4 v[UNROLL];
 #pragma unroll
       for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(s + i + u * kThreads);
@@ -147,7 +154,7 @@ __global__ __launch_bounds__(kThreads) void permute_byte_kernel(const uint8_t *_
                                                                 size_t chunk_bytes, int prio,
                                                                 KTrace tr) {
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (int c = 0; c < nchunks; ++c) {
     const uint8_t *s = src + (size_t)pt.p[c] * chunk_bytes;
@@ -174,6 +181,16 @@ int clamp_wgs(size_t work_units, int wanted) {
   return (int)(wanted < (long long)cap ? wanted : cap);
 }
 
+// Period (10 ns ticks) between a wave's trips so that the whole grid moves
+// trip_bytes per period, i.e. streams at rate_gbs; 0 = unpaced.
+uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
+  if (!(rate_gbs > 0.0)) return 0;
+  double t = trip_bytes / (rate_gbs * 1e9) * 1e8;
+  if (t < 1.0) t = 1.0;
+  if (t > 4.0e9) t = 4.0e9;
+  return (uint32_t)t;
+}
+
 }  // namespace
 
 int reduce_default_wgs(const ReduceCall &c) {
@@ -197,12 +214,15 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
     size_t nvec = c.len / 4;
     if (nvec > 0) {
       int g = clamp_wgs(nvec, wgs);
+      // positions per lane per trip of each instantiation
+      const int unroll = c.nchunks == 2 ? 4 : c.nchunks == 4 ? 2 : 1;
+      const uint32_t pace = pace_ticks((double)g * kThreads * unroll * 16.0 * (c.nchunks + 1), c.rate_gbs);
       switch (c.nchunks) {
-        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
-        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
-        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
-        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
-        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, c.trace); break;
+        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
+        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
+        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
+        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
+        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
       }
     }
     size_t first = nvec * 4;
@@ -242,9 +262,10 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     int parts = permute_parts(c.chunk_bytes);
     long long items = (long long)c.nchunks * parts;
     int g = (int)(wgs < items ? wgs : items);
+    const uint32_t pace = pace_ticks((double)g * kThreads * 4 * 16.0 * 2.0, c.rate_gbs);
     hipLaunchKernelGGL((permute_vec_kernel<4>), dim3(g), dim3(kThreads), 0, s,
                        static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
-                       c.chunk_bytes / 16, parts, c.priority, c.trace);
+                       c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
   } else {
     int g = clamp_wgs(c.chunk_bytes, wgs);
     hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kThreads), 0, s,

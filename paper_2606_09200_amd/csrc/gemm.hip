@@ -140,7 +140,7 @@ __global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__res
                                                            int prio, KTrace tr) {
   extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / T::WN;
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
                                                         KTrace tr) {
   extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
   constexpr int S = T::STAGES;
   constexpr int PER_STAGE = T::A_LOADS + T::B_LOADS;
   static_assert(T::ROWS_PER_PASS % 16 == 0, "a lane's swizzle must not change between passes");
@@ -462,7 +462,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(const uint16_t 
   extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
   (void)pad_lds;
   set_wave_priority(prio);
-  const uint64_t t0 = trace_begin(tr);
+  const TraceStart t0 = trace_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int r = lane & 15;   // A row / B row (output column) this lane feeds

@@ -49,6 +49,7 @@ struct ReduceCall {
   int wgs;                   // 0 = default
   int priority;              // 0..3
   KTrace trace;
+  double rate_gbs;           // target bandwidth of the vector path, GB/s; 0 = unpaced
 };
 int reduce_launch(const ReduceCall &c, hipStream_t s);
 int reduce_default_wgs(const ReduceCall &c);
@@ -62,6 +63,7 @@ struct PermuteCall {
   int wgs;
   int priority;
   KTrace trace;
+  double rate_gbs;           // as ReduceCall::rate_gbs
 };
 int permute_launch(const PermuteCall &c, hipStream_t s);
 int permute_default_wgs(const PermuteCall &c);

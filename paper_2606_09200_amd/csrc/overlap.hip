@@ -75,14 +75,19 @@ struct Launcher {
     c.trace = t;
     return gemm_launch(c, s);
   }
-  int comm(hipStream_t s, KTrace t) {
+  // `paced`: the overlapped schedule's launches stream at rate_gbs (the
+  // sequential schedule and the isolated timings always run unpaced).
+  double rate_gbs;
+  int comm(hipStream_t s, KTrace t, bool paced) {
     if (kind == OCC_COMM_REDUCE) {
       ReduceCall c = r;
       c.trace = t;
+      c.rate_gbs = paced ? rate_gbs : 0.0;
       return reduce_launch(c, s);
     }
     PermuteCall c = p;
     c.trace = t;
+    c.rate_gbs = paced ? rate_gbs : 0.0;
     return permute_launch(c, s);
   }
 };
@@ -95,6 +100,8 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c->gemm_grid < 0 || c->gemm_variant < 0) return OCC_EINVAL;
   if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO | OCC_RUN_GRAPH)) != 0) return OCC_EINVAL;
   if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
+  if (!(c->comm_rate_gbs == 0.0 || (c->comm_rate_gbs >= OCC_MIN_COMM_RATE_GBS && c->comm_rate_gbs <= 1.0e6)))
+    return OCC_EINVAL;
   OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K));
   size_t cbytes = (size_t)c->M * c->N * 2;
   // K_g writes C while K_c runs: C must not overlap anything K_c touches,
@@ -134,7 +141,7 @@ namespace {
 int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KTrace &off) {
   for (int i = 0; i < n; ++i) {
     OCC_TRY(L.gemm(s0, off));
-    OCC_TRY(L.comm(s0, off));
+    OCC_TRY(L.comm(s0, off, false));
   }
   return OCC_OK;
 }
@@ -147,7 +154,7 @@ int enqueue_ovl(Launcher &L, hipStream_t s0, hipStream_t s1, hipEvent_t fork, hi
     OCC_TRY(L.gemm(s0, tg[i]));
     OCC_HIP(hipEventRecord(deps[i], s0));
     OCC_HIP(hipStreamWaitEvent(s1, deps[i], 0));
-    OCC_TRY(L.comm(s1, tc[i]));
+    OCC_TRY(L.comm(s1, tc[i], true));
   }
   // C_{n-1} waits on G_{n-1}, the last GEMM, so the comm stream's end is the
   // end of the schedule; the compute stream waits for it.
@@ -187,8 +194,9 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   const KTrace off{nullptr, nullptr, 0, 0};
   L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
                  c.gemm_priority, off};
-  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off};
-  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off};
+  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
+  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
+  L.rate_gbs = c.comm_rate_gbs;
 
   occ_gemm_plan plan;
   OCC_TRY(gemm_plan(L.g, &plan));
@@ -268,7 +276,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
       for (int i = 0; i < n && st == OCC_OK; ++i) {
         st = L.gemm(s0, off);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 1], s0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK) st = L.comm(s0, off);
+        if (st == OCC_OK) st = L.comm(s0, off, false);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 2], s0) != hipSuccess) st = OCC_EHIP;
       }
       OCC_HIP(hipEventSynchronize(iso[2 * n]));

@@ -8,7 +8,8 @@ the reduction 100*(1 - TimeRatio) (Section 4.2), the isolated kernel times
 with the GEMM's MFMA fraction and the comm kernel's HBM fraction, the GEMM's
 resident workgroups per CU (Section 3.1), the overlap rate (Section 4.2) and
 the fraction of comm workgroups that shared a CU with a running GEMM
-workgroup (from the per-workgroup trace).
+workgroup, and the GEMM workgroups' mean lifetime and engine clock with and
+without a collective running (from the per-workgroup trace).
 """
 import argparse
 import json
@@ -22,37 +23,11 @@ import torch  # noqa: E402
 
 from paper_2606_09200_amd import binding as occ  # noqa: E402
 from paper_2606_09200_amd import inputs  # noqa: E402
+from paper_2606_09200_amd import trace  # noqa: E402
 from paper_2606_09200_amd.workloads import BLOCK_COUNTS, WORKLOADS  # noqa: E402
 
 PEAK_TFLOPS = 2500.0
 PEAK_GBS = 8000.0
-
-
-def overlap_rate(tl, n):
-    t = tl.cpu().tolist()
-    g = [(t[4 * i], t[4 * i + 1]) for i in range(n)]
-    c = [(t[4 * i + 2], t[4 * i + 3]) for i in range(n)]
-    tot = sum(e - s for s, e in c)
-    both = sum(max(0, min(ce, ge) - max(cs, gs)) for cs, ce in c for gs, ge in g)
-    return both / tot if tot else 0.0
-
-
-def coresidency(wt):
-    """Fraction of comm workgroups that ran on a CU while a GEMM workgroup did."""
-    recs = occ.decode_wg_trace(wt)
-    if not recs:
-        return None
-    a = np.array([[r["tag"] & 1, r["xcc"] * 64 + r["se"] * 16 + r["sh"] * 8 + r["cu"], r["t0"], r["t1"]]
-                  for r in recs], dtype=np.int64)
-    g = a[a[:, 0] == 0]
-    c = a[a[:, 0] == 1]
-    if len(c) == 0:
-        return None
-    hit = 0
-    for cu, s, e in c[:, 1:]:
-        m = (g[:, 1] == cu) & (g[:, 2] < e) & (g[:, 3] > s)
-        hit += bool(m.any())
-    return hit / len(c)
 
 
 def setup(w, dev):
@@ -79,10 +54,13 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
     if not plan["feasible"]:
         return row
     tl = torch.zeros(4 * w.n_iter, dtype=torch.int64, device=dev)
-    wt = torch.zeros(4 + 8 * 60000, dtype=torch.int32, device=dev)
+    wt = torch.zeros(4 + occ.WG_RECORD_WORDS * 60000, dtype=torch.int32, device=dev)
     r = occ.run_overlap(A, B, C, lds_bytes=pad, comm_priority=prio, n_iter=w.n_iter, reps=reps,
                         warmup=warmup, timeline=tl, wg_trace=wt, flags=flags, **knobs, **comm)
     tg, tc = r["t_gemm_ms"], r["t_comm_ms"]
+    g_iv, c_iv = trace.intervals(tl.cpu(), w.n_iter)
+    recs = occ.decode_wg_trace(wt)
+    inter = trace.interference(recs, c_iv)
     row.update({
         "t_seq_ms": round(r["t_seq_ms"], 4), "t_ovl_ms": round(r["t_ovl_ms"], 4),
         "reduction_pct": round(r["reduction_pct"], 2),
@@ -95,8 +73,12 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
         "comm_gbs": round(w.comm_bytes / tc / 1e6, 1),
         "comm_hbm_frac": round(w.comm_bytes / tc / 1e6 / PEAK_GBS, 4),
         "comm_wgs": r["comm_wgs"],
-        "overlap_rate": round(overlap_rate(tl, w.n_iter), 4),
-        "comm_coresident": coresidency(wt),
+        "overlap_rate": round(trace.overlap_rate(g_iv, c_iv), 4),
+        "comm_coresident": trace.coresidency(recs),
+        "gemm_wg_us_alone": inter.get("alone", {}).get("mean_us"),
+        "gemm_wg_us_with_comm": inter.get("with_comm", {}).get("mean_us"),
+        "gemm_clock_ghz_alone": inter.get("alone", {}).get("clock_ghz"),
+        "gemm_clock_ghz_with_comm": inter.get("with_comm", {}).get("clock_ghz"),
     })
     return row
 
@@ -104,7 +86,8 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 def table(rows):
     cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
-            "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident"]
+            "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
+            "gemm_wg_us_with_comm", "gemm_clock_ghz_alone", "gemm_clock_ghz_with_comm"]
     out = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
     for r in rows:
         out.append("| " + " | ".join("" if r.get(c) is None else

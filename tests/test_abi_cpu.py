@@ -113,6 +113,15 @@ def test_run_overlap_argument_errors(L):
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
     cfg.flags = 64
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.flags = 0
+    cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    for rate in (-1.0, 5.0, float("nan"), 1e7):                          # pacing out of range
+        cfg.comm_rate_gbs = rate
+        assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1, rate
+    assert b.MIN_COMM_RATE_GBS == 10.0
+    for rate in (0.0, 10.0, 1500.0):                                      # valid: passes validation
+        cfg.comm_rate_gbs = rate
+        assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1, rate
 
 
 def test_overlap_tune_argument_errors(L):

@@ -152,3 +152,63 @@ def test_graph_replays_match_eager(kind):
         assert r["t_seq_ms"] > 0 and r["t_ovl_ms"] > 0
         assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16)), call
         assert torch.equal(comm[outk].view(torch.uint8), ref.view(torch.uint8)), call
+
+
+def test_wg_trace_records_every_workgroup():
+    """One record per workgroup of every kernel of the traced pass, tagged
+    with its iteration and kind, on a real CU and XCD, with an engine clock
+    (cycles over elapsed 10 ns ticks) in the chip's range."""
+    n = 3
+    A, B, C, chunks, out = tiny_reduce_setup(M=2048, N=2048, K=2048, nchunks=4, length=1 << 22)
+    cap = 8192
+    wt = torch.zeros(4 + occ.WG_RECORD_WORDS * cap, dtype=torch.int32, device=DEV)
+    r = occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=n, reps=1, warmup=0, comm_wgs=64,
+                        wg_trace=wt)
+    torch.cuda.synchronize()
+    grid = occ.occ_gemm_plan_query(2048, 2048, 2048)["grid"]
+    assert r["comm_wgs"] == 64
+    assert int(wt[0]) == n * (grid + 64) <= cap
+    recs = occ.decode_wg_trace(wt)
+    for i in range(n):
+        g = [x for x in recs if x["tag"] == 2 * i]
+        c = [x for x in recs if x["tag"] == 2 * i + 1]
+        assert len(g) == grid and sorted(x["block"] for x in g) == list(range(grid))
+        assert len(c) == 64 and sorted(x["block"] for x in c) == list(range(64))
+        assert all(x["kind"] == "gemm" for x in g) and all(x["kind"] == "comm" for x in c)
+        # the collective of iteration i starts after the GEMM of iteration i ended
+        assert min(x["t0"] for x in c) >= max(x["t1"] for x in g)
+    assert all(x["t1"] >= x["t0"] and x["xcc"] < 8 for x in recs)
+    ticks = sum(x["t1"] - x["t0"] for x in recs)
+    cycles = sum(x["cycles"] for x in recs)
+    ghz = cycles / (ticks * 10.0)
+    assert 0.5 < ghz < 3.0, ghz
+
+
+@pytest.mark.parametrize("kind", ["reduce", "permute"])
+def test_paced_collective_keeps_results_and_rate(kind):
+    """comm_rate_gbs paces the overlapped schedule's collective: results stay
+    bit-identical, the sequential schedule stays unpaced, and the overlapped
+    makespan is at least the paced transfer time of its n collectives."""
+    n = 2
+    A, B = inputs.gemm_operands(512, 512, 512, seed=0, device=DEV)
+    C = torch.empty((512, 512), device=DEV, dtype=torch.bfloat16)
+    if kind == "reduce":
+        chunks = inputs.reduce_chunks(4, 1 << 20, seed=1, device=DEV)
+        ref = torch.empty(1 << 20, device=DEV)
+        occ.share_reduce(chunks, ref)
+        comm = dict(bufs=chunks, out=torch.empty_like(ref), comm_wgs=16)
+        outk, nbytes, rate = "out", 5 * 4 * (1 << 20), 20.0
+    else:
+        src = inputs.permute_payload(16, 1 << 16, seed=2, device=DEV)
+        perm = inputs.chunk_permutation(16, seed=3)
+        ref = torch.empty_like(src)
+        occ.share_permute(src, ref, perm, 1 << 16)
+        comm = dict(src=src, dst=torch.empty_like(src), perm=perm, chunk_bytes=1 << 16, comm_wgs=4)
+        outk, nbytes, rate = "dst", 2 * 16 * (1 << 16), 10.0
+    torch.cuda.synchronize()
+    r = occ.run_overlap(A, B, C, n_iter=n, reps=2, warmup=1, comm_priority=0, comm_rate_gbs=rate, **comm)
+    torch.cuda.synchronize()
+    assert torch.equal(comm[outk].view(torch.uint8), ref.view(torch.uint8))
+    paced_ms = nbytes / (rate * 1e9) * 1e3
+    assert r["t_ovl_ms"] >= 0.8 * n * paced_ms, (r, paced_ms)
+    assert r["t_comm_ms"] < 0.5 * paced_ms and r["t_seq_ms"] < r["t_ovl_ms"], r
