@@ -74,6 +74,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
         "comm_hbm_frac": round(w.comm_bytes / tc / 1e6 / PEAK_GBS, 4),
         "comm_wgs": r["comm_wgs"],
         "overlap_rate": round(trace.overlap_rate(g_iv, c_iv), 4),
+        "comm_ovl_us": round(sum(e - s for s, e in c_iv) / len(c_iv) * trace.TICK_NS / 1e3, 1),
         "comm_coresident": trace.coresidency(recs),
         "gemm_wg_us_alone": inter.get("alone", {}).get("mean_us"),
         "gemm_wg_us_with_comm": inter.get("with_comm", {}).get("mean_us"),
@@ -84,9 +85,10 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 
 
 def table(rows):
-    cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
+    cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
+            "comm_rate_gbs", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
-            "t_comm_ms", "comm_hbm_frac", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
+            "t_comm_ms", "comm_hbm_frac", "comm_ovl_us", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
             "gemm_wg_us_with_comm", "gemm_clock_ghz_alone", "gemm_clock_ghz_with_comm"]
     out = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
     for r in rows:
@@ -106,6 +108,12 @@ def main(argv=None):
                     help="also run occ_overlap_tune per workload and report its choice")
     ap.add_argument("--workloads", default="tiny,cb,mb,a2a,sweep,blocks,paper_cb_ar,paper_mb_ar,"
                                            "paper_cb_a2a,paper_mb_a2a")
+    ap.add_argument("--comm-wgs", default="0",
+                    help="comma list of comm workgroup counts (0 = library default)")
+    ap.add_argument("--rates", default="0",
+                    help="comma list of comm bandwidth pacings in GB/s for the overlapped schedule (0 = off)")
+    ap.add_argument("--priorities", default=None,
+                    help="comma list of comm wave priorities (default: each workload's own)")
     a = ap.parse_args(argv)
     dev = "cuda:0"
     rows = []
@@ -122,19 +130,24 @@ def main(argv=None):
             points = [dict(gemm_variant=v) for v in (0, 25, 14, 7)]
         else:
             points = [dict(gemm_variant=0)]
+        prios = [int(x) for x in a.priorities.split(",")] if a.priorities else list(w.priorities)
+        extra = [dict(comm_wgs=int(cw), comm_rate_gbs=float(rt))
+                 for cw in a.comm_wgs.split(",") for rt in a.rates.split(",")]
         for knobs in points:
-            base = {}
-            for pad in w.pads:
-                for prio in w.priorities:
-                    row = measure(w, A, B, C, comm, pad, prio, dev,
-                                  flags=occ.OCC_RUN_GRAPH if a.graph else 0, **knobs)
-                    row["graph"] = bool(a.graph)
-                    if prio == 0:
-                        base[pad] = row.get("t_ovl_ms")
-                    elif base.get(pad) and row.get("t_ovl_ms"):
-                        row["norm_time"] = round(row["t_ovl_ms"] / base[pad], 4)
-                    rows.append(row)
-                    print(json.dumps(row), flush=True)
+            for ex in extra:
+                base = {}
+                for pad in w.pads:
+                    for prio in prios:
+                        row = measure(w, A, B, C, comm, pad, prio, dev,
+                                      flags=occ.OCC_RUN_GRAPH if a.graph else 0, **knobs, **ex)
+                        row["graph"] = bool(a.graph)
+                        row["comm_rate_gbs"] = ex["comm_rate_gbs"]
+                        if prio == 0:
+                            base[pad] = row.get("t_ovl_ms")
+                        elif base.get(pad) and row.get("t_ovl_ms"):
+                            row["norm_time"] = round(row["t_ovl_ms"] / base[pad], 4)
+                        rows.append(row)
+                        print(json.dumps(row), flush=True)
         if a.tune and name not in ("sweep", "blocks"):
             knobs, r, prefer_seq = occ.occ_overlap_tune(A, B, C, n_iter=w.n_iter, reps=5, warmup=2,
                                                         tune_reps=3, **comm)

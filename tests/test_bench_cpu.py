@@ -30,3 +30,16 @@ def test_help_lists_the_knobs():
     for k in ("--steps", "--warmup", "--workload", "--pad-kib", "--priority", "--variant", "--gemm-grid",
               "--comm-wgs", "--comm-rate-gbs", "--cpu-budget", "--no-cpu-baseline"):
         assert k in p.stdout, k
+
+
+def test_sweep_table_renders_partial_rows():
+    sys.path.insert(0, ROOT)
+    from paper_2606_09200_amd import sweep
+    rows = [{"workload": "cb", "gemm_variant": 16, "pad_kib": 0, "comm_priority": 0, "t_seq_ms": 10.5,
+             "t_ovl_ms": 9.7, "comm_coresident": 0.9},
+            {"workload": "sweep", "pad_kib": 128, "comm_priority": 3, "feasible": False}]
+    t = sweep.table(rows).splitlines()
+    assert len(t) == 4 and t[0].startswith("| workload |")
+    ncol = t[0].count("|")
+    assert all(line.count("|") == ncol for line in t)
+    assert "| 0.900 |" in t[2] and "| 9.7 |" in t[2]
