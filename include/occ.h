@@ -99,7 +99,13 @@ enum {
   OCC_GEMM_DLP_256x128x32_4W_2ST = 24,
   OCC_GEMM_DLP_128x256x32_4W_2ST = 25,
   OCC_GEMM_DLP_256x128x32_4W_3ST = 26,
-  OCC_GEMM_DLP_128x256x32_4W_3ST = 27
+  OCC_GEMM_DLP_128x256x32_4W_3ST = 27,
+  /* skinny (M <= 16) with each wave's K-slice of A held in registers: B is
+     the only operand streamed per 16-column unit.  K must be a positive
+     multiple of 2048 and at most 8192 (28) / 4096 (29); automatic choice for
+     such K when M <= 16. */
+  OCC_GEMM_SKINNY_AREG_K8192 = 28,
+  OCC_GEMM_SKINNY_AREG_K4096 = 29
 };
 
 /*
@@ -109,9 +115,10 @@ enum {
  * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
  * and the pad never change the result.  The tiled variants (1-7, 9-19, 24-27)
  * accumulate every output over k in the same order and give bit-identical
- * results; the skinny variants (8, 20-23) split K across waves and may differ
- * from them, and from each other, in the last bit.  OCC_EINVAL for an unknown
- * variant or a skinny variant with M > 16.
+ * results; the skinny variants (8, 20-23, 28, 29) split K across waves and
+ * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
+ * an unknown variant, a skinny variant with M > 16, or a K that variant 28/29
+ * does not take.
  */
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);

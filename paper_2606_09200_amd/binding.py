@@ -31,8 +31,9 @@ GEMM_VARIANTS = {
     20: "skinny 8w u16", 21: "skinny 8w u8", 22: "skinny 4w u8", 23: "skinny 16w u8",
     24: "dl+pipe 256x128x32 4w 2st 2wg/cu", 25: "dl+pipe 128x256x32 4w 2st 2wg/cu",
     26: "dl+pipe 256x128x32 4w 3st 2wg/cu", 27: "dl+pipe 128x256x32 4w 3st 2wg/cu",
+    28: "skinny A-in-registers K<=8192", 29: "skinny A-in-registers K<=4096",
 }
-SKINNY_VARIANTS = (8, 20, 21, 22, 23)
+SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 

@@ -538,6 +538,110 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kernel(const uint16_t 
   trace_end(tr, t0);
 }
 
+// Skinny kernel with A held in registers (M <= 16; K a multiple of
+// 64 * WAVES * UNROLL and at most WAVES * KBW * 32).  The same unit, lane
+// layout and wave split of K as gemm_skinny_kernel, but each wave loads its
+// K-slice of the 16 A rows into registers once (K / (32 * WAVES) 32-wide
+// k-blocks, 4 registers each) and keeps it for every unit it processes, so a
+// unit streams only its 16 B rows: half the bytes per unit through the memory
+// pipeline.  Every k-block is whole, so loads need no bounds checks: a lane
+// whose A or B row is past M or N reads row 0 instead and feeds only an output
+// row or column that is not stored.  B loads run one chunk (UNROLL k-blocks)
+// ahead of the MFMAs that consume them, across unit boundaries too (the even
+// chunk count puts the next unit's first chunk in the free buffer).  Partial
+// sums are added in wave order through a double-buffered LDS array, one
+// barrier per unit.
+template <int WAVES, int KBW, int UNROLL>
+__global__ __launch_bounds__(64 * WAVES) void gemm_skinny_areg_kernel(const uint16_t *__restrict__ A,
+                                                                      const uint16_t *__restrict__ B,
+                                                                      uint16_t *__restrict__ C, int M,
+                                                                      int N, int K, int prio,
+                                                                      KTrace tr) {
+  static_assert(KBW % (2 * UNROLL) == 0, "k-blocks per wave must be an even number of chunks");
+  constexpr int NCH = KBW / UNROLL;
+  __shared__ f32x4 partial[2][WAVES - 1][64];
+  extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
+  (void)pad_lds;
+  set_wave_priority(prio);
+  const TraceStart t0 = trace_begin(tr);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int r = lane & 15;
+  const int g = lane >> 4;
+  const int bpw = K / (kSkinnyKB * WAVES);  // k-blocks per wave, <= KBW (checked by the host)
+  const int nch = bpw / UNROLL;             // chunks, even (checked by the host)
+  const int units = (N + 15) / 16;
+  // Wave w owns the contiguous K-slice [w * bpw * 32, (w + 1) * bpw * 32):
+  // separate sequential streams per wave spread over the HBM channels better
+  // (measured) than interleaving the waves' chunks.
+  const int kbase = wave * bpw * kSkinnyKB + g * 8;
+
+  u32x4 a[KBW];
+  {
+    const uint16_t *arow = A + (size_t)(r < M ? r : 0) * K + kbase;
+#pragma unroll
+    for (int j = 0; j < KBW; ++j) {
+      u32x4 z = {0u, 0u, 0u, 0u};
+      if (j < bpw) z = *reinterpret_cast<const u32x4 *>(arow + j * kSkinnyKB);
+      a[j] = z;
+    }
+  }
+  auto row_of = [&](int unit) { return B + (size_t)(unit * 16 + r < N ? unit * 16 + r : 0) * K + kbase; };
+  auto load_chunk = [&](const uint16_t *brow, int ch, u32x4(&bv)[UNROLL]) {
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u)
+      bv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(brow + (ch * UNROLL + u) * kSkinnyKB));
+  };
+
+  u32x4 bv[2][UNROLL];
+  if (blockIdx.x < units && nch > 0) load_chunk(row_of(blockIdx.x), 0, bv[0]);
+  int par = 0;
+  for (int unit = blockIdx.x; unit < units; unit += gridDim.x, par ^= 1) {
+    const uint16_t *brow = row_of(unit);
+    const int next = unit + (int)gridDim.x;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      if (ch < nch) {
+        if (ch + 1 < nch) {
+          if (ch + 1 < NCH) load_chunk(brow, ch + 1, bv[(ch + 1) & 1]);
+        } else if (next < units) {
+          load_chunk(row_of(next), 0, bv[(ch + 1) & 1]);  // (ch + 1) & 1 == 0: nch is even
+        }
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[ch * UNROLL + u]),
+                                                        __builtin_bit_cast(bf16x8, bv[ch & 1][u]), acc, 0, 0, 0);
+      }
+    }
+
+    // partial[par] was last read by wave 0 two units ago, before it reached
+    // the previous unit's barrier, which every writer has passed since
+    if (wave > 0) partial[par][wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave == 0) {
+      f32x4 s = acc;
+#pragma unroll
+      for (int w = 0; w < WAVES - 1; ++w) {
+        f32x4 p = partial[par][w][lane];
+        s[0] = s[0] + p[0];
+        s[1] = s[1] + p[1];
+        s[2] = s[2] + p[2];
+        s[3] = s[3] + p[3];
+      }
+      const int n = unit * 16 + r;
+      if (n < N) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          int m = 4 * g + i;
+          if (m < M) C[(size_t)m * N + n] = to_bf16(s[i]);
+        }
+      }
+    }
+  }
+  trace_end(tr, t0);
+}
+
 // ---------------------------------------------------------------------------
 // Variant table.
 typedef void (*TiledFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, int,
@@ -551,22 +655,31 @@ struct Variant {
   TiledFn fn;        // tiled kernels
   SkinnyFn skinny;   // skinny kernels (M <= 16)
   const char *name;
+  int kmax;          // largest K the kernel takes (0 = any)
+  int kmult;         // K must be a multiple of this (0 = any)
 };
 
 template <class T>
 constexpr Variant make_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name, 0, 0};
 }
 
 template <class T>
 constexpr Variant make_dl_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name, 0, 0};
 }
 
 template <int WAVES, int UNROLL>
 constexpr Variant make_skinny_variant(int id, const char *name) {
   return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, (WAVES - 1) * 64 * 16, nullptr,
-                 gemm_skinny_kernel<WAVES, UNROLL>, name};
+                 gemm_skinny_kernel<WAVES, UNROLL>, name, 0, 0};
+}
+
+template <int WAVES, int KBW, int UNROLL>
+constexpr Variant make_skinny_areg_variant(int id, const char *name) {
+  return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, 2 * (WAVES - 1) * 64 * 16, nullptr,
+                 gemm_skinny_areg_kernel<WAVES, KBW, UNROLL>, name, WAVES * KBW * kSkinnyKB,
+                 2 * WAVES * kSkinnyKB * UNROLL};
 }
 
 using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
@@ -624,7 +737,11 @@ const Variant kVariants[] = {
     make_dl_variant<P128x256k32_4w_2s>(25, "dl+pipe 128x256x32 4w 2st"),
     make_dl_variant<P256x128k32_4w_3s>(26, "dl+pipe 256x128x32 4w 3st"),
     make_dl_variant<P128x256k32_4w_3s>(27, "dl+pipe 128x256x32 4w 3st"),
+    make_skinny_areg_variant<8, 32, 4>(28, "skinny M<=16, A in registers, 8 waves, K<=8192, K%2048==0"),
+    make_skinny_areg_variant<8, 16, 4>(29, "skinny M<=16, A in registers, 8 waves, K<=4096, K%2048==0"),
 };
+
+constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
 
@@ -637,8 +754,13 @@ const Variant *find_variant(int id) {
 int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 int auto_variant(int M, int N, int K, int num_cus) {
-  (void)K;
-  if (M <= 16) return 21;  // skinny, 8 waves, 8 k-blocks in flight
+  if (M <= 16) {
+    // skinny, 8 waves; A kept in registers when K is whole 2048-wide slices
+    // that fit, else 8 k-blocks of A and B in flight per lane
+    if (K >= 2048 && K % 2048 == 0 && K <= 4096) return 29;
+    if (K >= 2048 && K % 2048 == 0 && K <= 8192) return 28;
+    return 21;
+  }
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
   if (big >= num_cus) return 16;
   long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
@@ -653,6 +775,9 @@ static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_g
   if (v == nullptr) return OCC_EINVAL;
   const bool skinny = is_skinny(v);
   if (skinny && c.M > 16) return OCC_EINVAL;
+  if (v->kmax > 0 && c.K > v->kmax) return OCC_EINVAL;
+  if (v->kmult > 0 && (c.K == 0 || c.K % v->kmult != 0)) return OCC_EINVAL;
+  if (v->id < 0 || v->id > kMaxVariantId) return OCC_EINVAL;
   p->tile_m = v->bm;
   p->tile_n = v->bn;
   p->tile_k = v->bk;
@@ -702,7 +827,7 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
   uint16_t *C = static_cast<uint16_t *>(c.C);
   if (v->fn) {
     int dyn = v->lds + (int)c.lds_bytes;
-    static bool attr_set[32] = {};
+    static bool attr_set[kMaxVariantId + 1] = {};
     if (!attr_set[v->id]) {
       if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -714,7 +839,7 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
     hipLaunchKernelGGL(v->fn, dim3(p.grid), dim3(v->threads), dyn, s, A, B, C, c.M, c.N, c.K,
                        tiles_m, tiles_n, c.priority, c.trace);
   } else {
-    static bool attr_set_skinny[32] = {};
+    static bool attr_set_skinny[kMaxVariantId + 1] = {};
     if (!attr_set_skinny[v->id]) {
       if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->skinny),
                               hipFuncAttributeMaxDynamicSharedMemorySize,

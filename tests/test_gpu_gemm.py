@@ -12,6 +12,7 @@ pytestmark = pytest.mark.gpu
 
 TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 24, 25, 26, 27]
 SKINNY = [8, 20, 21, 22, 23]
+AREG = {28: 8192, 29: 4096}   # skinny with A in registers: largest K (K % 2048 == 0)
 
 
 def run_gemm(A, B, lds_bytes=0, variant=0, grid_cap=0):
@@ -32,7 +33,8 @@ def int_operands(M, N, K, seed):
 
 
 @pytest.mark.parametrize("M,N,K", [(512, 512, 512), (300, 200, 136), (1, 1, 8), (17, 33, 64),
-                                   (257, 129, 520), (64, 64, 32), (16, 1000, 1032), (5, 77, 256)])
+                                   (257, 129, 520), (64, 64, 32), (16, 1000, 1032), (5, 77, 256),
+                                   (16, 1000, 2048), (7, 333, 6144), (3, 100, 5120)])
 def test_gemm_auto_full_parity(M, N, K):
     A, B = inputs.gemm_operands(M, N, K, seed=0)
     got = run_gemm(A, B)
@@ -58,6 +60,41 @@ def test_gemm_integer_operands_bit_exact(variant):
     A, B = int_operands(M, 150, 512, seed=variant)
     got = run_gemm(A, B, variant=variant)
     assert np.array_equal(got, oracle.gemm_bf16(A, B, M, 150, 512))
+
+
+@pytest.mark.parametrize("variant", sorted(AREG))
+@pytest.mark.parametrize("M,N", [(16, 260), (1, 17), (13, 1000)])
+def test_gemm_skinny_areg_full_parity(variant, M, N):
+    for K in range(2048, AREG[variant] + 1, 2048):
+        A, B = inputs.gemm_operands(M, N, K, seed=variant + K)
+        got = run_gemm(A, B, variant=variant)
+        ref = oracle.gemm_bf16(A, B, M, N, K)
+        assert_gemm_close(got, ref, 1.0, 1.0, K, "variant %d %dx%dx%d" % (variant, M, N, K))
+
+
+@pytest.mark.parametrize("variant", sorted(AREG))
+def test_gemm_skinny_areg_integer_bit_exact_and_invariant(variant):
+    A, B = int_operands(11, 150, 2048, seed=variant)
+    base = run_gemm(A, B, variant=variant)
+    assert np.array_equal(base, oracle.gemm_bf16(A, B, 11, 150, 2048))
+    for cap in (1, 7):
+        assert np.array_equal(run_gemm(A, B, variant=variant, grid_cap=cap), base), cap
+    assert np.array_equal(run_gemm(A, B, variant=variant, lds_bytes=32 << 10), base)
+
+
+@pytest.mark.parametrize("variant", sorted(AREG))
+def test_gemm_skinny_areg_rejects_unsupported_k(variant):
+    for K in (1032, 512, 1024, 3072, AREG[variant] + 2048):
+        A, B = inputs.gemm_operands(16, 64, K, seed=1, device=DEV)
+        C = torch.empty((16, 64), device=DEV, dtype=torch.bfloat16)
+        with pytest.raises(occ.OccError) as e:
+            occ.occ_gemm_ex(A, B, C, variant=variant)
+        assert e.value.status == occ.OCC_EINVAL, K
+    with pytest.raises(occ.OccError):
+        occ.occ_gemm_plan_query(16, 64, 0, 0, variant)          # K = 0: not this kernel
+    assert occ.occ_gemm_plan_query(16, 64, 4096, 0, 0)["kernel_id"] == 29
+    assert occ.occ_gemm_plan_query(16, 64, 8192, 0, 0)["kernel_id"] == 28
+    assert occ.occ_gemm_plan_query(16, 64, 8200, 0, 0)["kernel_id"] == 21
 
 
 def test_gemm_identity_and_ones():
@@ -148,7 +185,7 @@ def test_gemm_full_size_skinny_full_parity():
     w = WORKLOADS["mb"]
     A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=DEV)
     ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), w.M, w.N, w.K)
-    for v in [0] + SKINNY:
+    for v in [0] + SKINNY + [28]:
         C = torch.full((w.M, w.N), float("nan"), device=DEV, dtype=torch.bfloat16)
         occ.occ_gemm_ex(A, B, C, variant=v)
         torch.cuda.synchronize()
