@@ -1,0 +1,219 @@
+// Direct-to-LDS tiled GEMM kernel (included by gemm.hip only).
+#pragma once
+
+#include "gemm_common.h"
+
+namespace occ {
+namespace {
+
+// ---------------------------------------------------------------------------
+// Direct-to-LDS kernel.  Same tile, LDS layout, MFMA loop and epilogue as
+// gemm_tiled_kernel, but each k-step of A and B goes from HBM straight into
+// LDS with buffer_load_dwordx4 ... lds: no staging registers, no LDS store
+// instructions, STAGES-1 k-steps in flight.  A lane's 16 bytes land at
+// M0 + 16*lane, so each lane fetches the logical chunk that the XOR swizzle
+// places at its slot.  Buffer range checking supplies the zeros: rows past
+// M (N) lie beyond the tile panel's num_records, and chunks past K get an
+// offset beyond any panel.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ i32x4 make_rsrc(const void *base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = (int)(uint32_t)a;
+  r[1] = (int)((a >> 32) & 0xFFFFu);  // stride 0: raw buffer, byte offsets
+  r[2] = (int)bytes;                  // num_records: loads at offset >= bytes return 0
+  r[3] = 0x00020000;                  // data format for untyped buffer access
+  r[0] = __builtin_amdgcn_readfirstlane(r[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(r[2]);
+  return r;
+}
+
+// One 16-byte-per-lane DMA into LDS at M0 + 16*lane.  Issued through asm so
+// that the wait for it is explicit (wait_vmcnt) rather than a conservative
+// full drain before every later LDS read.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, uint32_t lds_addr, uint32_t voff) {
+  // lds_addr and rsrc are wave-uniform; readfirstlane puts them in SGPRs.
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(rsrc)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// Wait until at most `ahead` later stages (of `per_stage` loads each) are
+// still in flight.
+template <int MAXAHEAD, int PER_STAGE>
+__device__ __forceinline__ void wait_stages(int ahead) {
+  if constexpr (MAXAHEAD <= 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= MAXAHEAD) wait_vmcnt<MAXAHEAD * PER_STAGE>();
+    else wait_stages<MAXAHEAD - 1, PER_STAGE>(ahead);
+  }
+}
+
+template <class T>
+__global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t *__restrict__ A,
+                                                        const uint16_t *__restrict__ B,
+                                                        uint16_t *__restrict__ C, int M, int N,
+                                                        int K, int tiles_m, int tiles_n, int prio,
+                                                        KTrace tr) {
+  extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
+  set_wave_priority(prio);
+  const TraceStart t0 = trace_begin(tr);
+  constexpr int S = T::STAGES;
+  constexpr int PER_STAGE = T::A_LOADS + T::B_LOADS;
+  static_assert(T::ROWS_PER_PASS % 16 == 0, "a lane's swizzle must not change between passes");
+  constexpr int ROW_BYTES = T::BK * 2;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / T::WN;
+  const int wn = wave % T::WN;
+  const int ntiles = tiles_m * tiles_n;
+  const int nk = (K + T::BK - 1) / T::BK;
+  const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) unsigned char *)smem;
+
+  // This lane's slot in every load pass: row r_in of the pass, physical
+  // chunk q; the swizzle is the same for all passes of a lane, so one offset
+  // (plus k0) serves every pass: each pass gets a buffer descriptor of its
+  // own, based at the pass's first row, whose num_records covers only the
+  // pass's rows that exist.
+  const int r_in = threadIdx.x / T::KCH;
+  const int q = threadIdx.x % T::KCH;
+  const int c = q ^ (swz<T::KCH>(r_in, 0));
+  const uint32_t lane_off = (uint32_t)r_in * (uint32_t)K * 2u + (uint32_t)c * 16u;
+  const uint32_t wave_lds = (uint32_t)wave * 1024u;
+
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    int tm, tn;
+    tile_coords<8>(xcd_remap(t, ntiles), tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * T::BM;
+    const int n0 = tn * T::BN;
+
+    auto pass_rsrc = [&](const uint16_t *base, int row0, int rows) {
+      const int have = min(T::ROWS_PER_PASS, max(0, rows - row0));
+      return make_rsrc(base + (size_t)row0 * K, (uint32_t)have * (uint32_t)K * 2u);
+    };
+    auto issue = [&](int kt) {
+      const int k0 = kt * T::BK;
+      const uint32_t sbase = lds0 + (uint32_t)((kt % S) * T::STAGE_BYTES) + wave_lds;
+      const uint32_t v = (k0 + c * 8 < K) ? lane_off + (uint32_t)k0 * 2u : 0x80000000u;
+#pragma unroll
+      for (int p = 0; p < T::A_LOADS; ++p)
+        lds_dma16(pass_rsrc(A, m0 + p * T::ROWS_PER_PASS, M), sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), v);
+#pragma unroll
+      for (int p = 0; p < T::B_LOADS; ++p)
+        lds_dma16(pass_rsrc(B, n0 + p * T::ROWS_PER_PASS, N),
+                  sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES), v);
+    };
+
+    f32x16 acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+#pragma unroll
+    for (int s = 0; s < S - 1; ++s)
+      if (s < nk) issue(s);
+
+    const int arow = wm * T::TM + (lane & 31);
+    const int brow = wn * T::TN + (lane & 31);
+    const int half = lane >> 5;
+
+    for (int kt = 0; kt < nk; ++kt) {
+      // k-step kt has landed once at most min(S-2, nk-1-kt) later steps are
+      // outstanding; the barrier then publishes it and retires step kt-1.
+      wait_stages<S - 2, PER_STAGE>(min(S - 2, nk - 1 - kt));
+      __syncthreads();
+      if (kt + S - 1 < nk) issue(kt + S - 1);
+
+      // Fragments of 16-wide k-substep ks+1 are read from LDS while the MFMAs
+      // of substep ks run (two register sets); the scheduling groups below
+      // interleave one LDS read after each MFMA.
+      const unsigned char *cur = smem + (kt % S) * T::STAGE_BYTES;
+      constexpr int KS = T::BK / 16;
+      bf16x8 af[2][T::FM], bfr[2][T::FN];
+      auto load_frags = [&](int ks, bf16x8(&fa)[T::FM], bf16x8(&fb)[T::FN]) {
+        const int cc = ks * 2 + half;
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i) {
+          int r = arow + i * 32;
+          fa[i] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4 *>(cur + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
+        }
+        const unsigned char *bs = cur + T::A_BYTES;
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) {
+          int r = brow + j * 32;
+          fb[j] = __builtin_bit_cast(
+              bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
+        }
+      };
+      load_frags(0, af[0], bfr[0]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) load_frags(ks + 1, af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
+#pragma unroll
+        for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < T::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][i], bfr[ks & 1][j], acc[i][j], 0, 0, 0);
+      }
+      if constexpr (T::PIPE) {
+        constexpr int NF = T::FM + T::FN;      // LDS reads per substep
+        constexpr int NMF = T::FM * T::FN;     // MFMAs per substep
+        __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks + 1 < KS) {
+#pragma unroll
+            for (int x = 0; x < NF; ++x) {
+              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            if constexpr (NMF > NF) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NF, 0);
+          } else {
+            __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();  // every wave is done with the stages before the next tile's prologue
+
+    const int ncol = lane & 31;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j) {
+        const int n = n0 + wn * T::TN + j * 32 + ncol;
+        const int mb = m0 + wm * T::TM + i * 32 + 4 * half;
+        if (n < N) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = mb + 8 * (r >> 2) + (r & 3);
+            if (m < M) C[(size_t)m * N + n] = to_bf16(acc[i][j][r]);
+          }
+        }
+        // keep the accumulator reads of one block next to its stores (the
+        // scheduler would otherwise hoist all of them and exhaust registers)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+  }
+  trace_end(tr, t0);
+}
+
+}  // namespace
+}  // namespace occ
