@@ -179,6 +179,20 @@ def main():
     recs = occ.decode_wg_trace(wt)
     inter = trace.interference(recs, c_iv)
     cores = trace.coresidency(recs)
+    resid = trace.residency(recs)
+
+    # a plain 1 GiB device-to-device copy: a measured HBM ceiling beside the spec peak
+    src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
 
     gemm_tflops = w.gemm_flops / (r["t_gemm_ms"] * 1e-3) / 1e12
     comm_gbs = w.comm_bytes / (r["t_comm_ms"] * 1e-3) / 1e9
@@ -230,6 +244,10 @@ def main():
         },
         "t_seq_ms": round(r["t_seq_ms"], 4),
         "t_ovl_ms": round(r["t_ovl_ms"], 4),
+        "t_seq_median_ms": round(r["t_seq_median_ms"], 4),
+        "t_ovl_median_ms": round(r["t_ovl_median_ms"], 4),
+        "t_seq_std_ms": round(r["t_seq_std_ms"], 4),
+        "t_ovl_std_ms": round(r["t_ovl_std_ms"], 4),
         "time_ratio": round(r["t_ovl_ms"] / r["t_seq_ms"], 4),
         "t_gemm_ms": round(r["t_gemm_ms"], 4),
         "t_comm_ms": round(r["t_comm_ms"], 4),
@@ -238,8 +256,11 @@ def main():
         "gemm_mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
         "comm_gbs": round(comm_gbs, 1),
         "comm_hbm_frac": round(comm_gbs / PEAK_HBM_GBS, 4),
+        "hbm_copy_gbs": round(copy_gbs, 1),
+        "comm_copy_frac": round(comm_gbs / copy_gbs, 4),
         "overlap_rate": round(overlap_rate, 4),
         "comm_coresident": None if cores is None else round(cores, 4),
+        "gemm_wg_per_cu_achieved": resid,
         "gemm_wg": inter,
         "t_ovl_normal_priority_ms": round(r_lo["t_ovl_ms"], 4),
         "reduction_pct_normal_priority": round(100.0 * (1.0 - r_lo["t_ovl_ms"] / r["t_seq_ms"]), 3),

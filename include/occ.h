@@ -262,6 +262,8 @@ typedef struct occ_overlap_result {
   int gemm_grid;          /* GEMM workgroups per launch */
   int gemm_tile_lds;      /* S_tile, bytes */
   int comm_wgs;           /* comm workgroups per launch */
+  double t_seq_median_ms, t_ovl_median_ms;  /* median over the timed repetitions */
+  double t_seq_std_ms, t_ovl_std_ms;        /* sample standard deviation (0 for reps = 1) */
 } occ_overlap_result;
 
 /*

@@ -71,7 +71,8 @@ class occ_overlap_result(ctypes.Structure):
     _fields_ = [(n, ctypes.c_double) for n in (
         "t_seq_ms", "t_ovl_ms", "t_seq_min_ms", "t_ovl_min_ms", "reduction_pct", "t_gemm_ms",
         "t_comm_ms")] + [(n, ctypes.c_int) for n in (
-            "gemm_wg_per_cu", "gemm_grid", "gemm_tile_lds", "comm_wgs")]
+            "gemm_wg_per_cu", "gemm_grid", "gemm_tile_lds", "comm_wgs")] + [(n, ctypes.c_double) for n in (
+                "t_seq_median_ms", "t_ovl_median_ms", "t_seq_std_ms", "t_ovl_std_ms")]
 
 
 _lib = None

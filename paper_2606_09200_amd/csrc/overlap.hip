@@ -16,6 +16,8 @@
 
 #include <string.h>
 
+#include <algorithm>
+#include <cmath>
 #include <vector>
 
 namespace occ {
@@ -163,6 +165,18 @@ int enqueue_ovl(Launcher &L, hipStream_t s0, hipStream_t s1, hipEvent_t fork, hi
   return OCC_OK;
 }
 
+// Median and sample standard deviation (0 for a single value) of the timed
+// repetitions.
+void median_and_std(std::vector<double> v, double mean, double *median, double *sd) {
+  if (v.empty()) return;
+  std::sort(v.begin(), v.end());
+  const size_t n = v.size();
+  *median = n % 2 ? v[n / 2] : 0.5 * (v[n / 2 - 1] + v[n / 2]);
+  double ss = 0;
+  for (double x : v) ss += (x - mean) * (x - mean);
+  *sd = n > 1 ? std::sqrt(ss / (double)(n - 1)) : 0.0;
+}
+
 struct Graph {
   hipGraph_t g = nullptr;
   hipGraphExec_t x = nullptr;
@@ -239,6 +253,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   }
 
   double seq_sum = 0, ovl_sum = 0, seq_min = 1e300, ovl_min = 1e300, g_sum = 0, c_sum = 0;
+  std::vector<double> seq_t, ovl_t;  // per timed repetition, for median and spread
   int st = OCC_OK;
   for (int rep = 0; rep < c.warmup + c.reps && st == OCC_OK; ++rep) {
     const bool timed = rep >= c.warmup;
@@ -254,6 +269,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
       if (timed) {
         seq_sum += ms;
         seq_min = ms < seq_min ? ms : seq_min;
+        seq_t.push_back(ms);
       }
     }
     if (flags & OCC_RUN_OVL) {
@@ -269,6 +285,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
       if (timed) {
         ovl_sum += ms;
         ovl_min = ms < ovl_min ? ms : ovl_min;
+        ovl_t.push_back(ms);
       }
     }
     if (flags & OCC_RUN_ISO) {
@@ -320,10 +337,12 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   if (flags & OCC_RUN_SEQ) {
     res->t_seq_ms = seq_sum / R;
     res->t_seq_min_ms = seq_min;
+    median_and_std(seq_t, res->t_seq_ms, &res->t_seq_median_ms, &res->t_seq_std_ms);
   }
   if (flags & OCC_RUN_OVL) {
     res->t_ovl_ms = ovl_sum / R;
     res->t_ovl_min_ms = ovl_min;
+    median_and_std(ovl_t, res->t_ovl_ms, &res->t_ovl_median_ms, &res->t_ovl_std_ms);
   }
   if ((flags & OCC_RUN_SEQ) && (flags & OCC_RUN_OVL) && res->t_seq_ms > 0)
     res->reduction_pct = 100.0 * (1.0 - res->t_ovl_ms / res->t_seq_ms);

@@ -76,6 +76,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
         "overlap_rate": round(trace.overlap_rate(g_iv, c_iv), 4),
         "comm_ovl_us": round(sum(e - s for s, e in c_iv) / len(c_iv) * trace.TICK_NS / 1e3, 1),
         "comm_coresident": trace.coresidency(recs),
+        "gemm_wg_per_cu_achieved": (trace.residency(recs) or {}).get("median"),
         "gemm_wg_us_alone": inter.get("alone", {}).get("mean_us"),
         "gemm_wg_us_with_comm": inter.get("with_comm", {}).get("mean_us"),
         "gemm_clock_ghz_alone": inter.get("alone", {}).get("clock_ghz"),
@@ -86,7 +87,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 
 def table(rows):
     cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
-            "comm_rate_gbs", "gemm_wg_per_cu", "t_seq_ms", "t_ovl_ms",
+            "comm_rate_gbs", "gemm_wg_per_cu", "gemm_wg_per_cu_achieved", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "comm_ovl_us", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
             "gemm_wg_us_with_comm", "gemm_clock_ghz_alone", "gemm_clock_ghz_with_comm"]

@@ -8,7 +8,9 @@ run_overlap records (occ_overlap_cfg.timeline / .wg_trace).
                         while a GEMM workgroup ran on the same CU;
 * ``interference``   -- GEMM workgroups split by whether a collective kernel
                         was running at the time: their mean lifetime and the
-                        engine clock they ran at (cycles / elapsed time).
+                        engine clock they ran at (cycles / elapsed time);
+* ``residency``      -- achieved residency: the most workgroups of one kind
+                        that ran at the same time on one CU.
 
 Clock ticks are the GPU's constant 100 MHz clock (10 ns); cycles are
 engine-clock cycles.
@@ -80,3 +82,25 @@ def interference(records, comm_spans):
         res[k] = {"n": d["n"], "mean_us": round(float(np.mean(d["dur"])), 2),
                   "clock_ghz": round(float(np.median(d["ghz"])), 3) if d["ghz"] else None}
     return res
+
+
+def residency(records, kind="gemm"):
+    """Achieved residency of ``kind`` workgroups: for every CU the largest
+    number of them alive at one instant (a workgroup ending at t does not
+    overlap one starting at t).  Returns {"median": m, "max": x, "cus": n}
+    over the CUs that ran any, or None."""
+    per = {}
+    for r in records:
+        if r["kind"] == kind:
+            per.setdefault(_cu_key(r), []).append((r["t0"], r["t1"]))
+    if not per:
+        return None
+    peaks = []
+    for ivs in per.values():
+        ev = sorted([(t0, 1) for t0, _ in ivs] + [(t1, -1) for _, t1 in ivs], key=lambda e: (e[0], e[1]))
+        cur = best = 0
+        for _, d in ev:
+            cur += d
+            best = max(best, cur)
+        peaks.append(best)
+    return {"median": float(np.median(peaks)), "max": int(max(peaks)), "cus": len(peaks)}

@@ -212,3 +212,15 @@ def test_paced_collective_keeps_results_and_rate(kind):
     paced_ms = nbytes / (rate * 1e9) * 1e3
     assert r["t_ovl_ms"] >= 0.8 * n * paced_ms, (r, paced_ms)
     assert r["t_comm_ms"] < 0.5 * paced_ms and r["t_seq_ms"] < r["t_ovl_ms"], r
+
+
+def test_makespan_statistics():
+    A, B, C, chunks, out = tiny_reduce_setup(M=1024, N=1024, K=1024, nchunks=4, length=1 << 20)
+    r = occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=4, reps=7, warmup=1)
+    for k in ("seq", "ovl"):
+        mean, med, lo, sd = r["t_%s_ms" % k], r["t_%s_median_ms" % k], r["t_%s_min_ms" % k], r["t_%s_std_ms" % k]
+        assert 0 < lo <= med and lo <= mean and sd >= 0
+        assert mean - lo <= 3 * sd * 7 ** 0.5 + 1e-9       # min lies within the sample's spread
+    r1 = occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=2, reps=1, warmup=0)
+    assert r1["t_seq_std_ms"] == 0 and r1["t_seq_median_ms"] == pytest.approx(r1["t_seq_ms"])
+    assert r1["t_ovl_median_ms"] == pytest.approx(r1["t_ovl_ms"]) == r1["t_ovl_min_ms"]

@@ -66,3 +66,14 @@ def test_interference_split_and_clock():
     assert out["with_comm"]["n"] == 1 and out["with_comm"]["mean_us"] == pytest.approx(3.0)
     assert out["with_comm"]["clock_ghz"] == pytest.approx(2.2)
     assert trace.interference(recs, []) ["alone"]["n"] == 3
+
+
+def test_residency_counts_simultaneous_workgroups_per_cu():
+    recs = [rec("gemm", 0, 0, 0, 10), rec("gemm", 0, 0, 5, 15), rec("gemm", 0, 0, 15, 20),  # peak 2
+            rec("gemm", 0, 1, 0, 10), rec("gemm", 0, 1, 10, 20),                           # back to back: 1
+            rec("gemm", 1, 0, 0, 10), rec("gemm", 1, 0, 1, 9), rec("gemm", 1, 0, 2, 8),   # peak 3
+            rec("comm", 0, 0, 0, 100)]
+    r = trace.residency(recs)
+    assert r == {"median": 2.0, "max": 3, "cus": 3}
+    assert trace.residency(recs, "comm") == {"median": 1.0, "max": 1, "cus": 1}
+    assert trace.residency([], "gemm") is None
