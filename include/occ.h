@@ -308,7 +308,11 @@ int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *re
 /* Static string naming a status code. */
 const char *occ_strerror(int status);
 
-/* Library version, (major << 16) | minor. */
+/* Library version, (major << 16) | minor.  The minor number grows whenever a
+   structure above gains fields, so a binding can refuse a library whose
+   layout it does not know. */
+#define OCC_VERSION_MAJOR 1
+#define OCC_VERSION_MINOR 1
 int occ_version(void);
 
 #ifdef __cplusplus

@@ -34,6 +34,7 @@ GEMM_VARIANTS = {
     28: "skinny A-in-registers K<=8192", 29: "skinny A-in-registers K<=4096",
 }
 SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
+ABI_VERSION = (1, 1)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -109,6 +110,10 @@ def lib():
             f = getattr(L, name)
             f.argtypes = args
             f.restype = ctypes.c_char_p if name == "occ_strerror" else ctypes.c_int
+        v = L.occ_version()
+        if (v >> 16, v & 0xFFFF) != ABI_VERSION:
+            raise RuntimeError("%s has ABI version %d.%d, this binding expects %d.%d; rebuild it with "
+                               "python -m paper_2606_09200_amd.build" % ((LIB_PATH, v >> 16, v & 0xFFFF) + ABI_VERSION))
         _lib = L
     return _lib
 

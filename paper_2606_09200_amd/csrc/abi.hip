@@ -168,6 +168,6 @@ const char *occ_strerror(int status) {
   }
 }
 
-int occ_version(void) { return (1 << 16) | 0; }
+int occ_version(void) { return (OCC_VERSION_MAJOR << 16) | OCC_VERSION_MINOR; }
 
 }  // extern "C"

@@ -39,7 +39,9 @@ def test_strerror_and_version(L):
     for code in range(0, -7, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == (1, 0)
+    assert binding.occ_version() == binding.ABI_VERSION == (1, 1)
+    hdr = open(HEADER).read()
+    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 1" in hdr
 
 
 P = ctypes.c_void_p
