@@ -162,7 +162,8 @@ int share_reduce(const float *const *bufs, int nchunks, size_t len, float *out, 
 
 /*
  * share_reduce_ex -- share_reduce with the comm-kernel knobs: `wgs`
- * workgroups (0 = library default) and wave priority `priority` in 0..3
+ * workgroups (0 = library default: one per CU, fewer for short inputs) and
+ * wave priority `priority` in 0..3
  * (s_setprio; 0 = normal).  Same result for every wgs and priority.
  */
 int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *out, int wgs,
@@ -292,7 +293,7 @@ int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
  * runtime policy the paper leaves to future work (Section 6).  Times the
  * overlapped schedule of *cfg (tune_reps repetitions after one warm-up) for
  * every candidate in
- *   comm_priority {0, 3} x comm_wgs {library default, one per CU}
+ *   comm_priority {0, 3} x comm_wgs {library default (one per CU), two per CU}
  *   x gemm_grid {one workgroup per tile, one persistent workgroup per CU}
  *   x lds_bytes {0, the pad that lowers the GEMM's residency by one
  *                workgroup per CU (only when it has more than one)},

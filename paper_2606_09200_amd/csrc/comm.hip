@@ -30,8 +30,10 @@ struct ChunkPtrs {
 // sum is acc = c0[j]; acc = acc + c1[j]; ... exactly in chunk order; the
 // loads of all chunks for UNROLL positions are issued before any addition.
 // Measured on MI355X: for 8 chunks, one position per trip (8 loads in flight
-// per lane, 52 VGPRs) at 2 workgroups per CU streams fastest (5.9 TB/s);
-// deeper unrolling adds registers without adding bandwidth.
+// per lane, 52 VGPRs) streams 5.3-5.9 TB/s; deeper unrolling adds registers
+// without adding bandwidth.  The default grid is one workgroup per CU (one
+// wave per SIMD): as fast as two per CU alone, and a co-running GEMM loses
+// less issue time to one comm wave per SIMD than to two.
 template <int NC, int UNROLL>
 __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
                                                               float *__restrict__ out, int prio,
@@ -196,7 +198,7 @@ uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
 int reduce_default_wgs(const ReduceCall &c) {
   const DeviceInfo *di = nullptr;
   int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
-  return clamp_wgs(c.len / 4 + 1, 2 * cus);
+  return clamp_wgs(c.len / 4 + 1, cus);
 }
 
 int reduce_launch(const ReduceCall &c, hipStream_t s) {
@@ -248,7 +250,7 @@ int permute_default_wgs(const PermuteCall &c) {
   const DeviceInfo *di = nullptr;
   int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
   long long items = (long long)c.nchunks * permute_parts(c.chunk_bytes);
-  long long want = 2LL * cus;
+  long long want = cus;
   return (int)(items < want ? items : want);
 }
 

@@ -356,7 +356,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
 // Adaptive choice of the occupancy and priority knobs (the runtime policy the
 // paper names as future work, Section 6): time the overlapped schedule for
 // each candidate and keep the fastest.  Candidates: comm wave priority
-// {0, 3} x comm workgroups {library default, one per CU} x GEMM grid {one
+// {0, 3} x comm workgroups {one per CU (the default), two per CU} x GEMM grid {one
 // workgroup per tile, persistent one per CU} x extra LDS pad {0, the pad
 // that lowers the GEMM's residency by one workgroup per CU, when one exists}.
 int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
@@ -385,7 +385,7 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
     }
   }
   const int prios[2] = {0, 3};
-  const int wgs[2] = {0, di->num_cus};
+  const int wgs[2] = {0, 2 * di->num_cus};
   const int grids[2] = {0, di->num_cus};
 
   occ_overlap_cfg c = *cfg;
