@@ -14,6 +14,8 @@
 
 #include <string.h>
 
+#include <type_traits>
+
 namespace occ {
 namespace {
 
@@ -34,27 +36,38 @@ struct ChunkPtrs {
 // without adding bandwidth.  The default grid is one workgroup per CU (one
 // wave per SIMD): as fast as two per CU alone, and a co-running GEMM loses
 // less issue time to one comm wave per SIMD than to two.
-template <int NC, int UNROLL>
+template <int NC, int UNROLL, bool OFF32>
 __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
                                                               float *__restrict__ out, int prio,
                                                               uint32_t pace, KTrace tr) {
+  // OFF32: every byte offset the loop forms fits in 32 bits (checked by the
+  // host), so each access is a scalar base plus one shared 32-bit lane
+  // offset instead of a 64-bit address per chunk: fewer vector instructions
+  // per byte, which is issue time a co-running GEMM on the same SIMD gets back.
+  using I = typename std::conditional<OFF32, uint32_t, size_t>::type;
   set_wave_priority(prio);
   const TraceStart t0 = trace_begin(tr);
   Pacer pc = pace_start(pace);
   const int nc = NC > 0 ? NC : nchunks;
-  const size_t stride = (size_t)gridDim.x * kThreads;
-  size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
-  f32x4 *o = reinterpret_cast<f32x4 *>(out);
+  const I n = (I)nvec;
+  const I stride = (I)gridDim.x * kThreads;
+  I i = (I)blockIdx.x * kThreads + threadIdx.x;
+  auto ld = [&](int c, I k) {
+    return __builtin_nontemporal_load(
+        reinterpret_cast<const f32x4 *>(reinterpret_cast<const char *>(cp.p[c]) + k * (I)sizeof(f32x4)));
+  };
+  auto st = [&](f32x4 v, I k) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(reinterpret_cast<char *>(out) + k * (I)sizeof(f32x4)));
+  };
 
   if constexpr (NC > 0) {
-    for (bool first = true; i + (UNROLL - 1) * stride < nvec; i += UNROLL * stride, first = false) {
+    for (bool first = true; i + (UNROLL - 1) * stride < n; i += UNROLL * stride, first = false) {
       if (!first) pace_wait(pc);
       f32x4 v[NC][UNROLL];
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int u = 0; u < UNROLL; ++u)
-          v[c][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[c]) + i + u * stride);
+        for (int u = 0; u < UNROLL; ++u) v[c][u] = ld(c, i + u * stride);
 #pragma unroll
       for (int u = 0; u < UNROLL; ++u) {
         f32x4 acc = v[0][u];
@@ -65,20 +78,20 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
           acc[2] = acc[2] + v[c][u][2];
           acc[3] = acc[3] + v[c][u][3];
         }
-        __builtin_nontemporal_store(acc, o + i + u * stride);
+        st(acc, i + u * stride);
       }
     }
   }
   // Remaining positions (and every position when the chunk count is only
   // known at run time): chunks in batches of 8 loads, folded in order.
-  for (bool first = true; i < nvec; i += stride, first = false) {
+  for (bool first = true; i < n; i += stride, first = false) {
     if (NC == 0 && !first) pace_wait(pc);
-    f32x4 acc = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[0]) + i);
+    f32x4 acc = ld(0, i);
     for (int c0 = 1; c0 < nc; c0 += 8) {
       f32x4 v[8];
 #pragma unroll
       for (int c = 0; c < 8; ++c)
-        if (c0 + c < nc) v[c] = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(cp.p[c0 + c]) + i);
+        if (c0 + c < nc) v[c] = ld(c0 + c, i);
 #pragma unroll
       for (int c = 0; c < 8; ++c)
         if (c0 + c < nc) {
@@ -88,7 +101,7 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
           acc[3] = acc[3] + v[c][3];
         }
     }
-    __builtin_nontemporal_store(acc, o + i);
+    st(acc, i);
   }
   trace_end(tr, t0);
 }
@@ -117,11 +130,14 @@ struct PermTable {
 // Permutation copy, 16-byte units.  Work item w covers part (w % parts) of
 // destination chunk (w / parts); workgroups stride over work items, threads
 // over the part's units with UNROLL loads in flight before the stores.
-template <int UNROLL>
+template <int UNROLL, bool OFF32>
 __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
                                                                u32x4 *__restrict__ dst, PermTable pt,
                                                                int nchunks, size_t cvec, int parts,
                                                                int prio, uint32_t pace, KTrace tr) {
+  // OFF32: offsets inside a chunk fit in 32 bits (checked by the host): the
+  // work item's chunk bases are scalar and the lanes share one 32-bit offset.
+  using I = typename std::conditional<OFF32, uint32_t, size_t>::type;
   set_wave_priority(prio);
   const TraceStart t0 = trace_begin(tr);
   Pacer pc = pace_start(pace);
@@ -130,21 +146,23 @@ __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__re
   for (int w = blockIdx.x; w < nwork; w += gridDim.x) {
     const int chunk = w / parts;
     const int part = w - chunk * parts;
-    const size_t lo = cvec * part / parts;
-    const size_t hi = cvec * (part + 1) / parts;
-    const u32x4 *s = src + (size_t)pt.p[chunk] * cvec;
-    u32x4 *d = dst + (size_t)chunk * cvec;
-    size_t i = lo + threadIdx.x;
+    const I lo = (I)(cvec * part / parts);
+    const I hi = (I)(cvec * (part + 1) / parts);
+    const char *s = reinterpret_cast<const char *>(src + (size_t)pt.p[chunk] * cvec);
+    char *d = reinterpret_cast<char *>(dst + (size_t)chunk * cvec);
+    auto at = [](const char *b, I k) { return reinterpret_cast<const u32x4 *>(b + k * (I)sizeof(u32x4)); };
+    auto atw = [](char *b, I k) { return reinterpret_cast<u32x4 *>(b + k * (I)sizeof(u32x4)); };
+    I i = lo + threadIdx.x;
     for (; i + (UNROLL - 1) * kThreads < hi; i += UNROLL * kThreads) {
       if (!first) pace_wait(pc);
       first = false;
       u32x4 v[UNROLL];
 #pragma unroll
-      for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(s + i + u * kThreads);
+      for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(at(s, i + u * kThreads));
 #pragma unroll
-      for (int u = 0; u < UNROLL; ++u) __builtin_nontemporal_store(v[u], d + i + u * kThreads);
+      for (int u = 0; u < UNROLL; ++u) __builtin_nontemporal_store(v[u], atw(d, i + u * kThreads));
     }
-    for (; i < hi; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+    for (; i < hi; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(at(s, i)), atw(d, i));
   }
   trace_end(tr, t0);
 }
@@ -195,6 +213,18 @@ uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
 
 }  // namespace
 
+template <bool OFF32>
+void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_t nvec, float *out, int prio,
+                   uint32_t pace, const KTrace &tr) {
+  switch (nchunks) {
+    case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+    case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 2, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+    case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+    case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+    default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+  }
+}
+
 int reduce_default_wgs(const ReduceCall &c) {
   const DeviceInfo *di = nullptr;
   int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
@@ -219,13 +249,11 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
       // positions per lane per trip of each instantiation
       const int unroll = c.nchunks == 2 ? 4 : c.nchunks == 4 ? 2 : 1;
       const uint32_t pace = pace_ticks((double)g * kThreads * unroll * 16.0 * (c.nchunks + 1), c.rate_gbs);
-      switch (c.nchunks) {
-        case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
-        case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 2>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
-        case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
-        case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
-        default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1>), dim3(g), dim3(kThreads), 0, s, cp, c.nchunks, nvec, c.out, prio, pace, c.trace); break;
-      }
+      // 32-bit offsets when the largest byte offset the loop can form, (nvec
+      // plus one unrolled grid stride) * 16, stays below 2^32
+      const bool off32 = ((double)nvec + 4.0 * g * kThreads) * 16.0 < 4294967296.0;
+      if (off32) launch_reduce<true>(c.nchunks, g, s, cp, nvec, c.out, prio, pace, c.trace);
+      else launch_reduce<false>(c.nchunks, g, s, cp, nvec, c.out, prio, pace, c.trace);
     }
     size_t first = nvec * 4;
     if (first < c.len)
@@ -265,9 +293,15 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     long long items = (long long)c.nchunks * parts;
     int g = (int)(wgs < items ? wgs : items);
     const uint32_t pace = pace_ticks((double)g * kThreads * 4 * 16.0 * 2.0, c.rate_gbs);
-    hipLaunchKernelGGL((permute_vec_kernel<4>), dim3(g), dim3(kThreads), 0, s,
-                       static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
-                       c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
+    // 32-bit offsets when a chunk plus one unrolled block stays below 2^32 bytes
+    if ((double)c.chunk_bytes + 4.0 * kThreads * 16.0 < 4294967296.0)
+      hipLaunchKernelGGL((permute_vec_kernel<4, true>), dim3(g), dim3(kThreads), 0, s,
+                         static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
+                         c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
+    else
+      hipLaunchKernelGGL((permute_vec_kernel<4, false>), dim3(g), dim3(kThreads), 0, s,
+                         static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
+                         c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
   } else {
     int g = clamp_wgs(c.chunk_bytes, wgs);
     hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kThreads), 0, s,
