@@ -153,3 +153,55 @@ def test_permute_workload_size_bit_exact():
     torch.cuda.synchronize()
     want = oracle.permute_chunks(src.cpu().numpy(), perm.numpy(), w.chunk_bytes)
     assert np.array_equal(dst.cpu().numpy(), want)
+
+
+# ------------------------------------------------------------ beyond 4 GiB
+def _sample_positions(n, seed, around=()):
+    rng = np.random.default_rng(seed)
+    idx = set(rng.integers(0, n, 4096).tolist())
+    idx.update(range(0, 64))
+    idx.update(range(max(0, n - 64), n))
+    for a in around:
+        idx.update(range(max(0, a - 64), min(n, a + 64)))
+    return torch.tensor(sorted(idx), dtype=torch.int64)
+
+
+def test_reduce_chunks_beyond_4gib_sampled():
+    """Chunks of 2^30 + 1027 floats (just over 4 GiB each): the kernel's byte
+    offsets no longer fit in 32 bits, so the 64-bit addressing path runs; the
+    scalar tail covers the last 3 elements.  Checked at sampled positions,
+    including both sides of the 2^32-byte boundary, against the oracle."""
+    n = (1 << 30) + 1027
+    g = torch.Generator(device=DEV)
+    g.manual_seed(11)
+    chunks = torch.rand((2, n), generator=g, device=DEV, dtype=torch.float32)
+    out = torch.full((n,), float("nan"), device=DEV)
+    occ.share_reduce(chunks, out)
+    torch.cuda.synchronize()
+    pos = _sample_positions(n, 1, around=((1 << 30), (1 << 28)))
+    p = pos.to(DEV)
+    got = out[p].cpu().numpy()
+    want = oracle.chunk_sum_f32(np.ascontiguousarray(chunks[:, p].cpu().numpy()))
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+    del chunks, out
+    torch.cuda.empty_cache()
+
+
+def test_permute_chunks_beyond_4gib_sampled():
+    """Two chunks of 4 GiB + 4096 B, swapped: 64-bit offsets inside a chunk."""
+    cb = (1 << 32) + 4096
+    src = torch.empty(2 * cb, dtype=torch.uint8, device=DEV)
+    g = torch.Generator(device=DEV)
+    g.manual_seed(12)
+    src.view(torch.int32).random_(generator=g)
+    dst = torch.zeros_like(src)
+    perm = torch.tensor([1, 0], dtype=torch.int32)
+    occ.share_permute(src, dst, perm, cb)
+    torch.cuda.synchronize()
+    pos = _sample_positions(cb, 2, around=((1 << 32),))
+    p = pos.to(DEV)
+    for i in range(2):
+        j = int(perm[i])
+        assert torch.equal(dst[i * cb + p], src[j * cb + p]), i
+    del src, dst
+    torch.cuda.empty_cache()
