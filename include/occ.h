@@ -117,8 +117,10 @@ enum {
  * accumulate every output over k in the same order and give bit-identical
  * results; the skinny variants (8, 20-23, 28, 29) split K across waves and
  * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
- * an unknown variant, a skinny variant with M > 16, or a K that variant 28/29
- * does not take.
+ * an unknown variant, a skinny variant with M > 16, a K that variant 28/29
+ * does not take, or K above 16 M (the direct-to-LDS variants 10-19, 24-27
+ * address a load pass with 32-bit offsets; for such K the automatic choice
+ * falls back to a register-staged variant).
  */
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);

@@ -44,9 +44,17 @@ constexpr Variant make_variant(int id, const char *name) {
   return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name, 0, 0};
 }
 
+// The direct-to-LDS kernel addresses a load pass with 32-bit byte offsets
+// (row within the pass * K * 2 + k * 2): K is capped so that they cannot wrap.
+template <class T>
+constexpr int dl_kmax() {
+  return (int)(((0xFFFFFFFFull / 2) / (unsigned long long)(T::ROWS_PER_PASS + 1)) & ~7ull);
+}
+
 template <class T>
 constexpr Variant make_dl_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name, 0, 0};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name,
+                 dl_kmax<T>(), 0};
 }
 
 template <int WAVES, int UNROLL>
@@ -142,7 +150,7 @@ int auto_variant(int M, int N, int K, int num_cus) {
     return 21;
   }
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
-  if (big >= num_cus) return 16;
+  if (big >= num_cus) return K <= find_variant(16)->kmax ? 16 : 3;  // 3: 64-bit addressing
   long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   if (mid >= num_cus / 2) return 5;
   return 7;

@@ -97,6 +97,17 @@ def test_gemm_skinny_areg_rejects_unsupported_k(variant):
     assert occ.occ_gemm_plan_query(16, 64, 8200, 0, 0)["kernel_id"] == 21
 
 
+def test_gemm_direct_to_lds_k_limit():
+    # 32-bit pass offsets: K above the variant's limit is refused, and the
+    # automatic choice for such K is a register-staged variant (plan only)
+    big = (1 << 25) + 8
+    with pytest.raises(occ.OccError) as e:
+        occ.occ_gemm_plan_query(4096, 4096, big, 0, 16)
+    assert e.value.status == occ.OCC_EINVAL
+    assert occ.occ_gemm_plan_query(4096, 4096, big)["kernel_id"] == 3
+    assert occ.occ_gemm_plan_query(4096, 4096, 1 << 20)["kernel_id"] == 16
+
+
 def test_gemm_identity_and_ones():
     A, _ = inputs.gemm_operands(96, 8, 128, seed=3)
     eye = torch.eye(128).to(torch.bfloat16)
