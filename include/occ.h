@@ -148,6 +148,17 @@ typedef struct occ_gemm_plan {
 int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                         occ_gemm_plan *plan);
 
+/*
+ * occ_gemm_info -- the three LDS figures of Section 3.1 for the kernel used
+ * on large shapes (variant 16): its tile's own LDS (S_tile), the device's
+ * per-workgroup LDS limit and its LDS per CU, in bytes; so a caller can
+ * size lds_bytes (S_tile + pad <= max_lds_per_wg; resident workgroups per CU
+ * <= lds_per_cu / (S_tile + pad)).  occ_gemm_plan_query gives the same for
+ * any shape and variant.  OCC_EINVAL for a null pointer; OCC_ENODEV without
+ * a gfx950 device.
+ */
+int occ_gemm_info(int *tile_lds_bytes, int *max_lds_per_wg, int *lds_per_cu);
+
 /* ------------------------------------------------------------------ K_c */
 
 /*

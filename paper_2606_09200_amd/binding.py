@@ -84,6 +84,7 @@ _SIGS = {
                     ctypes.c_int, ctypes.c_int, _P],
     "occ_gemm_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                             ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
+    "occ_gemm_info": [ctypes.POINTER(ctypes.c_int)] * 3,
     "share_reduce": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, _P],
     "share_reduce_ex": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, ctypes.c_int,
                         ctypes.c_int, _P],
@@ -178,6 +179,13 @@ def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=Fals
     d = {f: getattr(p, f) for f, _ in occ_gemm_plan._fields_}
     d["feasible"] = st == OCC_OK
     return d
+
+
+def occ_gemm_info():
+    """(S_tile of the large-shape kernel, max LDS per workgroup, LDS per CU), bytes."""
+    v = [ctypes.c_int(0) for _ in range(3)]
+    _check(lib().occ_gemm_info(*[ctypes.byref(x) for x in v]), "occ_gemm_info")
+    return tuple(x.value for x in v)
 
 
 def _chunk_ptrs(bufs):

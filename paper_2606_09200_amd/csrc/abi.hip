@@ -115,6 +115,19 @@ int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int 
   return occ::gemm_plan(c, plan);
 }
 
+int occ_gemm_info(int *tile_lds_bytes, int *max_lds_per_wg, int *lds_per_cu) {
+  if (tile_lds_bytes == nullptr || max_lds_per_wg == nullptr || lds_per_cu == nullptr) return OCC_EINVAL;
+  occ_gemm_plan p;
+  // the kernel the library picks for large shapes (any shape with at least
+  // one 256x256 tile per CU takes it)
+  int st = occ_gemm_plan_query(8192, 8192, 8192, 0, OCC_GEMM_DLP_256x256x64_8W_2ST, 0, &p);
+  if (st != OCC_OK) return st;
+  *tile_lds_bytes = p.tile_lds_bytes;
+  *max_lds_per_wg = p.max_lds_per_wg;
+  *lds_per_cu = p.lds_per_cu;
+  return OCC_OK;
+}
+
 int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *out, int wgs,
                     int priority, void *stream) {
   int st = occ::validate_reduce(bufs, nchunks, len, out);

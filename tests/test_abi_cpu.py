@@ -126,6 +126,13 @@ def test_run_overlap_argument_errors(L):
         assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1, rate
 
 
+def test_gemm_info_argument_errors(L):
+    x = ctypes.c_int(0)
+    assert L.occ_gemm_info(None, ctypes.byref(x), ctypes.byref(x)) == -1
+    assert L.occ_gemm_info(ctypes.byref(x), None, ctypes.byref(x)) == -1
+    assert L.occ_gemm_info(ctypes.byref(x), ctypes.byref(x), None) == -1
+
+
 def test_overlap_tune_argument_errors(L):
     from paper_2606_09200_amd import binding as b
     cfg = b.occ_overlap_cfg()

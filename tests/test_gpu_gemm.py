@@ -160,6 +160,13 @@ def test_gemm_rejects_infeasible_pad():
     assert e.value.status == occ.OCC_ELDS
 
 
+def test_gemm_info_matches_plan():
+    tile, max_wg, per_cu = occ.occ_gemm_info()
+    p = occ.occ_gemm_plan_query(8192, 8192, 8192, 0, 16)
+    assert (tile, max_wg, per_cu) == (p["tile_lds_bytes"], p["max_lds_per_wg"], p["lds_per_cu"])
+    assert tile == 2 * 64 * (256 + 256) * 2 and per_cu == 160 * 1024 and max_wg >= tile
+
+
 def test_occupancy_non_increasing_in_pad():
     for variant in (0, 5, 6, 7):
         prev = None
