@@ -126,7 +126,9 @@ def main(argv=None):
         # 128x256x32 (48 KiB, two per CU), 128x128x64 (96 KiB, three stages) and
         # the paper's opt2 64x64x64.
         if name == "blocks":
-            points = [dict(gemm_variant=6, gemm_grid=x * x) for x in BLOCK_COUNTS]
+            # the paper's two tiles (opt1 64x64x32, opt2 64x64x64) over the
+            # thread-block counts of its tile-size study
+            points = [dict(gemm_variant=v, gemm_grid=x * x) for v in (6, 7) for x in BLOCK_COUNTS]
         elif name == "sweep":
             points = [dict(gemm_variant=v) for v in (0, 25, 14, 7)]
         else:

@@ -14,8 +14,9 @@ collectives on 4-8 GPUs) become one GPU's local share of each collective:
                  chunk permutation (the local block of an alltoall);
 * ``sweep``   -- ``cb`` over extra LDS pads {0,16,32,64,96,128} KiB x comm wave
                  priority {normal, high};
-* ``blocks``  -- ``cb`` with the paper's opt1 tile and a persistent grid of X*X
-                 workgroups (the thread-block-count axis of Figs. 2-3);
+* ``blocks``  -- ``cb`` with the paper's opt1 and opt2 tiles and a persistent
+                 grid of X*X workgroups (the thread-block-count axis of
+                 Figs. 2-3 and the tile-size study of Section 4.3);
 * ``paper_*`` -- Table 1's own pairs on one GPU: cb (8192^3) and mb
                  (8192 x 57344 x 8192) GEMMs with an 896 MiB local share: a
                  4-chunk allreduce share (4 x 224 MiB fp32) or a 4-chunk
@@ -72,8 +73,9 @@ WORKLOADS = {
     "sweep": Workload("sweep", 8192, 8192, 8192, "reduce", 8, length=1 << 25,
                       pads=tuple(p * KIB for p in (0, 16, 32, 64, 96, 128)),
                       priorities=(0, 3)),
-    # the paper's thread-block-count axis (Figs. 2-3): cb with the opt1 tile and
-    # a persistent grid of X*X workgroups
+    # the paper's thread-block-count axis (Figs. 2-3) and tile-size study
+    # (Section 4.3): cb with the opt1 / opt2 tiles and a persistent grid of X*X
+    # workgroups
     "blocks": Workload("blocks", 8192, 8192, 8192, "reduce", 8, length=1 << 25,
                        priorities=(0, 3)),
 }
