@@ -209,7 +209,12 @@ enum { OCC_COMM_REDUCE = 0, OCC_COMM_PERMUTE = 1 };
    a HIP graph each and replay it per repetition, instead of issuing every
    kernel, event record and stream wait from the host (for schedules whose
    kernels are as short as the host's issue time). */
-enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4, OCC_RUN_GRAPH = 8 };
+enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4, OCC_RUN_GRAPH = 8, OCC_RUN_PACE_ALL = 16 };
+/* OCC_RUN_PACE_ALL: apply comm_rate_gbs to every schedule and to the isolated
+   timings, not only to the overlapped one.  This emulates on one GPU a
+   collective whose duration is set by inter-GPU links rather than by this
+   GPU's memory (the multi-GPU setting of Section 4): the local kernel then
+   streams at the link rate in the sequential schedule too. */
 
 typedef struct occ_overlap_cfg {
   /* K_g: as occ_gemm */
@@ -258,8 +263,9 @@ typedef struct occ_overlap_cfg {
      kernel streams at no more than this rate, leaving memory bandwidth to the
      co-running GEMM.  0 = unpaced (full speed); otherwise at least
      OCC_MIN_COMM_RATE_GBS.  The sequential schedule and the isolated kernel
-     timings always run unpaced, so t_seq stays the fastest sequential
-     makespan.  Results are unchanged (same arithmetic, same order). */
+     timings run unpaced, so t_seq stays the fastest sequential makespan,
+     unless flags has OCC_RUN_PACE_ALL.  Results are unchanged (same
+     arithmetic, same order). */
   double comm_rate_gbs;
 } occ_overlap_cfg;
 

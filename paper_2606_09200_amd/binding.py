@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libocc.so")
 
 OCC_OK, OCC_EINVAL, OCC_ELDS, OCC_EPERM, OCC_EALIAS, OCC_EHIP, OCC_ENODEV = 0, -1, -2, -3, -4, -5, -6
 OCC_COMM_REDUCE, OCC_COMM_PERMUTE = 0, 1
-OCC_RUN_SEQ, OCC_RUN_OVL, OCC_RUN_ISO, OCC_RUN_GRAPH = 1, 2, 4, 8
+OCC_RUN_SEQ, OCC_RUN_OVL, OCC_RUN_ISO, OCC_RUN_GRAPH, OCC_RUN_PACE_ALL = 1, 2, 4, 8, 16
 GEMM_VARIANTS = {
     0: "auto", 1: "256x256x64 4w", 2: "256x256x64 8w", 3: "256x128x64 4w",
     4: "256x128x64 4w 1-stage", 5: "128x128x64 4w", 6: "opt1 64x64x32", 7: "opt2 64x64x64",

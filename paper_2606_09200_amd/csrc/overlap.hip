@@ -77,10 +77,12 @@ struct Launcher {
     c.trace = t;
     return gemm_launch(c, s);
   }
-  // `paced`: the overlapped schedule's launches stream at rate_gbs (the
-  // sequential schedule and the isolated timings always run unpaced).
+  // `paced`: the overlapped schedule's launches stream at rate_gbs; the
+  // sequential schedule and the isolated timings do too when pace_all.
   double rate_gbs;
+  bool pace_all;
   int comm(hipStream_t s, KTrace t, bool paced) {
+    paced = paced || pace_all;
     if (kind == OCC_COMM_REDUCE) {
       ReduceCall c = r;
       c.trace = t;
@@ -100,7 +102,8 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c->comm_priority < 0 || c->comm_priority > 3 || c->comm_wgs < 0) return OCC_EINVAL;
   if (c->gemm_priority < 0 || c->gemm_priority > 3) return OCC_EINVAL;
   if (c->gemm_grid < 0 || c->gemm_variant < 0) return OCC_EINVAL;
-  if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO | OCC_RUN_GRAPH)) != 0) return OCC_EINVAL;
+  if ((c->flags & ~(OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO | OCC_RUN_GRAPH | OCC_RUN_PACE_ALL)) != 0)
+    return OCC_EINVAL;
   if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
   if (!(c->comm_rate_gbs == 0.0 || (c->comm_rate_gbs >= OCC_MIN_COMM_RATE_GBS && c->comm_rate_gbs <= 1.0e6)))
     return OCC_EINVAL;
@@ -199,7 +202,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   memset(res, 0, sizeof *res);
   const occ_overlap_cfg &c = *cfg;
   const int passes = c.flags & (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO);
-  const int flags = (passes ? passes : (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) | (c.flags & OCC_RUN_GRAPH);
+  const int flags = (passes ? passes : (OCC_RUN_SEQ | OCC_RUN_OVL | OCC_RUN_ISO)) |
+                    (c.flags & (OCC_RUN_GRAPH | OCC_RUN_PACE_ALL));
   const bool graph = (flags & OCC_RUN_GRAPH) != 0;
   const int n = c.n_iter;
 
@@ -211,6 +215,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
   L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
   L.rate_gbs = c.comm_rate_gbs;
+  L.pace_all = (c.flags & OCC_RUN_PACE_ALL) != 0;
 
   occ_gemm_plan plan;
   OCC_TRY(gemm_plan(L.g, &plan));
@@ -391,7 +396,7 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   occ_overlap_cfg c = *cfg;
   c.reps = tune_reps;
   c.warmup = 1;
-  c.flags = OCC_RUN_OVL | (cfg->flags & OCC_RUN_GRAPH);
+  c.flags = OCC_RUN_OVL | (cfg->flags & (OCC_RUN_GRAPH | OCC_RUN_PACE_ALL));
   c.timeline = nullptr;
   c.wg_trace = nullptr;
   double best = 1e300;

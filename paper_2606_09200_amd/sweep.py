@@ -86,7 +86,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 
 
 def table(rows):
-    cols = ["workload", "graph", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
+    cols = ["workload", "graph", "pace_all", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
             "comm_rate_gbs", "gemm_wg_per_cu", "gemm_wg_per_cu_achieved", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "comm_ovl_us", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
@@ -115,6 +115,9 @@ def main(argv=None):
                     help="comma list of comm bandwidth pacings in GB/s for the overlapped schedule (0 = off)")
     ap.add_argument("--priorities", default=None,
                     help="comma list of comm wave priorities (default: each workload's own)")
+    ap.add_argument("--pace-all", action="store_true",
+                    help="apply --rates to every schedule (OCC_RUN_PACE_ALL): emulates a collective "
+                         "whose time is set by inter-GPU links")
     a = ap.parse_args(argv)
     dev = "cuda:0"
     rows = []
@@ -141,9 +144,10 @@ def main(argv=None):
                 base = {}
                 for pad in w.pads:
                     for prio in prios:
-                        row = measure(w, A, B, C, comm, pad, prio, dev,
-                                      flags=occ.OCC_RUN_GRAPH if a.graph else 0, **knobs, **ex)
+                        fl = (occ.OCC_RUN_GRAPH if a.graph else 0) | (occ.OCC_RUN_PACE_ALL if a.pace_all else 0)
+                        row = measure(w, A, B, C, comm, pad, prio, dev, flags=fl, **knobs, **ex)
                         row["graph"] = bool(a.graph)
+                        row["pace_all"] = bool(a.pace_all)
                         row["comm_rate_gbs"] = ex["comm_rate_gbs"]
                         if prio == 0:
                             base[pad] = row.get("t_ovl_ms")

@@ -115,6 +115,8 @@ def test_run_overlap_argument_errors(L):
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
     cfg.flags = 64
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.flags = 16                                                        # OCC_RUN_PACE_ALL is valid
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1
     cfg.flags = 0
     cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
     for rate in (-1.0, 5.0, float("nan"), 1e7):                          # pacing out of range

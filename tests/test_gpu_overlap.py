@@ -224,3 +224,23 @@ def test_makespan_statistics():
     r1 = occ.run_overlap(A, B, C, bufs=chunks, out=out, n_iter=2, reps=1, warmup=0)
     assert r1["t_seq_std_ms"] == 0 and r1["t_seq_median_ms"] == pytest.approx(r1["t_seq_ms"])
     assert r1["t_ovl_median_ms"] == pytest.approx(r1["t_ovl_ms"]) == r1["t_ovl_min_ms"]
+
+
+def test_pace_all_paces_every_schedule():
+    """OCC_RUN_PACE_ALL: the sequential schedule and the isolated timing run
+    the collective paced too (link-bound emulation); results unchanged."""
+    A, B = inputs.gemm_operands(512, 512, 512, seed=0, device=DEV)
+    C = torch.empty((512, 512), device=DEV, dtype=torch.bfloat16)
+    chunks = inputs.reduce_chunks(4, 1 << 20, seed=1, device=DEV)
+    ref = torch.empty(1 << 20, device=DEV)
+    occ.share_reduce(chunks, ref)
+    out = torch.empty_like(ref)
+    rate = 20.0
+    paced_ms = 5 * 4 * (1 << 20) / (rate * 1e9) * 1e3
+    r = occ.run_overlap(A, B, C, bufs=chunks, out=out, comm_wgs=16, comm_priority=0, n_iter=2, reps=1,
+                        warmup=1, comm_rate_gbs=rate, flags=occ.OCC_RUN_SEQ | occ.OCC_RUN_OVL |
+                        occ.OCC_RUN_ISO | occ.OCC_RUN_PACE_ALL)
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
+    assert r["t_comm_ms"] >= 0.8 * paced_ms, r
+    assert r["t_seq_ms"] >= 0.8 * 2 * paced_ms and r["t_ovl_ms"] >= 0.8 * 2 * paced_ms, r
