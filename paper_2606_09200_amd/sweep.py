@@ -115,6 +115,10 @@ def main(argv=None):
                     help="comma list of comm bandwidth pacings in GB/s for the overlapped schedule (0 = off)")
     ap.add_argument("--priorities", default=None,
                     help="comma list of comm wave priorities (default: each workload's own)")
+    ap.add_argument("--gemm-grids", default=None,
+                    help="comma list of persistent GEMM grid caps to run each workload with "
+                         "(0 = one workgroup per tile); the rows then show the engine clock "
+                         "against the number of CUs the GEMM keeps busy")
     ap.add_argument("--pace-all", action="store_true",
                     help="apply --rates to every schedule (OCC_RUN_PACE_ALL): emulates a collective "
                          "whose time is set by inter-GPU links")
@@ -134,6 +138,8 @@ def main(argv=None):
             points = [dict(gemm_variant=v, gemm_grid=x * x) for v in (6, 7) for x in BLOCK_COUNTS]
         elif name == "sweep":
             points = [dict(gemm_variant=v) for v in (0, 25, 14, 7)]
+        elif a.gemm_grids:
+            points = [dict(gemm_variant=0, gemm_grid=int(g)) for g in a.gemm_grids.split(",")]
         else:
             points = [dict(gemm_variant=0)]
         prios = [int(x) for x in a.priorities.split(",")] if a.priorities else list(w.priorities)
