@@ -46,8 +46,15 @@ def _load():
         lib.oracle_double_to_bf16.restype = ctypes.c_uint16
         lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
         lib.oracle_bf16_to_double.restype = ctypes.c_double
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops run on in this process."""
+    return int(_load().oracle_num_threads())
 
 
 def _u16(x):

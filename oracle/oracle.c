@@ -31,6 +31,7 @@
 #include <stddef.h>
 #include <stdint.h>
 #include <string.h>
+#include <omp.h>
 
 #if FLT_EVAL_METHOD != 0
 #error "binary32 additions must not be evaluated in a wider format"
@@ -117,3 +118,6 @@ void oracle_permute(const uint8_t *src, uint8_t *dst, const int32_t *perm, int n
   for (int i = 0; i < nchunks; ++i)
     memcpy(dst + (size_t)i * chunk_bytes, src + (size_t)perm[i] * chunk_bytes, chunk_bytes);
 }
+
+/* Threads the parallel loops above use (OpenMP's limit for this process). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }

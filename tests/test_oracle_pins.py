@@ -268,3 +268,8 @@ def test_exact_rounding_helper_matches_torch_on_float32():
     for v, w in zip(x, want):
         assert rne_bf16_exact(Fraction(float(v))) == int(w)
     assert math.isfinite(float(bf16_value(0x7F7F)))
+
+
+def test_oracle_reports_its_thread_count():
+    # bench.py's cpu_baseline states the threads the oracle ran on
+    assert 1 <= oracle.num_threads() <= 4096
