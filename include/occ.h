@@ -105,7 +105,9 @@ enum {
      multiple of 2048 and at most 8192 (28) / 4096 (29); automatic choice for
      such K when M <= 16. */
   OCC_GEMM_SKINNY_AREG_K8192 = 28,
-  OCC_GEMM_SKINNY_AREG_K4096 = 29
+  OCC_GEMM_SKINNY_AREG_K4096 = 29,
+  /* B stored K x N (occ_gemm_kn / occ_gemm_kn_ex only) */
+  OCC_GEMM_KN_DLP_256x256x64_8W_2ST = 32
 };
 
 /*
@@ -125,6 +127,25 @@ enum {
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);
 
+/*
+ * occ_gemm_kn -- C = A * B with B stored K x N (row-major, N-contiguous):
+ *   C[m][n] = sum_k A[m][k] * B[k][n].  Same arithmetic, rounding and LDS pad
+ * as occ_gemm; the B tile is staged in LDS as stored and its MFMA operands
+ * are read with gfx950's LDS transpose reads.  Results are bit-identical to
+ * occ_gemm on the transposed B (same order of the k sums).
+ * Requirements: as occ_gemm, plus N % 8 == 0 (16-byte B rows) and N at
+ * most about 1.26e8 (a 16-row load pass of B is addressed with 32-bit
+ * offsets; larger N is OCC_EINVAL).
+ */
+int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                void *stream);
+
+/* occ_gemm_kn_ex -- occ_gemm_kn with a variant (0 = automatic, or
+   OCC_GEMM_KN_DLP_256x256x64_8W_2ST) and a grid cap as in occ_gemm_ex.
+   OCC_EINVAL for a variant that reads B as N x K. */
+int occ_gemm_kn_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                   int variant, int grid_cap, void *stream);
+
 /* Launch plan occ_gemm_ex would use, for reporting and sweeps. */
 typedef struct occ_gemm_plan {
   int tile_m, tile_n, tile_k;  /* output tile per workgroup and k-step */
@@ -141,7 +162,8 @@ typedef struct occ_gemm_plan {
 
 /*
  * occ_gemm_plan_query -- the plan for occ_gemm_ex(M, N, K, lds_bytes,
- * variant, grid_cap) on the current device.  Returns OCC_ELDS when
+ * variant, grid_cap) on the current device (for a K x N variant, the plan
+ * for occ_gemm_kn_ex).  Returns OCC_ELDS when
  * S_tile + lds_bytes exceeds the per-workgroup LDS limit (the plan is still
  * filled in, with wg_per_cu = 0).
  */
@@ -225,6 +247,7 @@ typedef struct occ_overlap_cfg {
   int gemm_variant;         /* OCC_GEMM_* (0 = automatic) */
   int gemm_grid;            /* 0: one workgroup per tile; > 0: persistent grid cap */
   int gemm_priority;        /* wave priority of the GEMM kernel, 0 (normal) .. 3 */
+  /* (gemm_b_layout is at the end of the structure) */
   /* K_c: as share_reduce (comm_kind 0) or share_permute (comm_kind 1) */
   int comm_kind;
   const float *const *bufs; /* host array of device pointers */
@@ -267,6 +290,8 @@ typedef struct occ_overlap_cfg {
      unless flags has OCC_RUN_PACE_ALL.  Results are unchanged (same
      arithmetic, same order). */
   double comm_rate_gbs;
+  /* layout of B: 0 = N x K (occ_gemm), 1 = K x N (occ_gemm_kn) */
+  int gemm_b_layout;
 } occ_overlap_cfg;
 
 #define OCC_MIN_COMM_RATE_GBS 10.0
@@ -332,7 +357,7 @@ const char *occ_strerror(int status);
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
 #define OCC_VERSION_MAJOR 1
-#define OCC_VERSION_MINOR 1
+#define OCC_VERSION_MINOR 2
 int occ_version(void);
 
 #ifdef __cplusplus

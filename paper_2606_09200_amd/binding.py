@@ -32,9 +32,11 @@ GEMM_VARIANTS = {
     24: "dl+pipe 256x128x32 4w 2st 2wg/cu", 25: "dl+pipe 128x256x32 4w 2st 2wg/cu",
     26: "dl+pipe 256x128x32 4w 3st 2wg/cu", 27: "dl+pipe 128x256x32 4w 3st 2wg/cu",
     28: "skinny A-in-registers K<=8192", 29: "skinny A-in-registers K<=4096",
+    32: "dl+pipe 256x256x64 8w 2st, B K x N",
 }
+KN_VARIANTS = (32,)       # take B stored K x N (occ_gemm_kn_ex only)
 SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
-ABI_VERSION = (1, 1)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+ABI_VERSION = (1, 2)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -64,7 +66,7 @@ class occ_overlap_cfg(ctypes.Structure):
         ("n_iter", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
         ("flags", ctypes.c_int), ("timeline", ctypes.c_void_p),
         ("wg_trace", ctypes.c_void_p), ("wg_trace_cap", ctypes.c_int),
-        ("comm_rate_gbs", ctypes.c_double),
+        ("comm_rate_gbs", ctypes.c_double), ("gemm_b_layout", ctypes.c_int),
     ]
 
 
@@ -82,6 +84,9 @@ _SIGS = {
     "occ_gemm": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
     "occ_gemm_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
                     ctypes.c_int, ctypes.c_int, _P],
+    "occ_gemm_kn": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
+    "occ_gemm_kn_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
+                       ctypes.c_int, ctypes.c_int, _P],
     "occ_gemm_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                             ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
     "occ_gemm_info": [ctypes.POINTER(ctypes.c_int)] * 3,
@@ -143,14 +148,14 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
 
 
-def _gemm_args(A, B, C):
+def _gemm_args(A, B, C, b_kn=False):
     for name, t in (("A", A), ("B", B), ("C", C)):
         if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 2:
             raise ValueError("%s must be a contiguous 2-D bfloat16 GPU tensor" % name)
     M, K = A.shape
-    N = B.shape[0]
-    if B.shape[1] != K or tuple(C.shape) != (M, N):
-        raise ValueError("shapes must be A (M,K), B (N,K), C (M,N)")
+    N = B.shape[1] if b_kn else B.shape[0]
+    if B.shape[0 if b_kn else 1] != K or tuple(C.shape) != (M, N):
+        raise ValueError("shapes must be A (M,K), B (%s), C (M,N)" % ("K,N" if b_kn else "N,K"))
     return M, N, K
 
 
@@ -166,6 +171,21 @@ def occ_gemm_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
     M, N, K = _gemm_args(A, B, C)
     _check(lib().occ_gemm_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
                              int(grid_cap), _stream(stream)), "occ_gemm_ex")
+    return C
+
+
+def occ_gemm_kn(A, B, C, lds_bytes=0, stream=None):
+    """C = A @ B (bf16, fp32 accumulation); B is K x N."""
+    M, N, K = _gemm_args(A, B, C, b_kn=True)
+    _check(lib().occ_gemm_kn(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), _stream(stream)),
+           "occ_gemm_kn")
+    return C
+
+
+def occ_gemm_kn_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
+    M, N, K = _gemm_args(A, B, C, b_kn=True)
+    _check(lib().occ_gemm_kn_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
+                                int(grid_cap), _stream(stream)), "occ_gemm_kn_ex")
     return C
 
 
@@ -254,14 +274,17 @@ def decode_wg_trace(wg_trace):
 
 def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant, gemm_grid,
               gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace,
-              comm_rate_gbs=0.0):
-    M, N, K = _gemm_args(A, B, C)
+              comm_rate_gbs=0.0, b_layout="nk"):
+    if b_layout not in ("nk", "kn"):
+        raise ValueError("b_layout must be 'nk' or 'kn'")
+    M, N, K = _gemm_args(A, B, C, b_kn=b_layout == "kn")
     cfg = occ_overlap_cfg()
     cfg.M, cfg.N, cfg.K = M, N, K
     cfg.A, cfg.B, cfg.C = _ptr(A).value, _ptr(B).value, _ptr(C).value
     cfg.lds_bytes, cfg.gemm_variant, cfg.gemm_grid = int(lds_bytes), int(gemm_variant), int(gemm_grid)
     cfg.gemm_priority = int(gemm_priority)
     cfg.comm_rate_gbs = float(comm_rate_gbs)
+    cfg.gemm_b_layout = 1 if b_layout == "kn" else 0
     keep = []
     if bufs is not None:
         arr, n, length = _chunk_ptrs(bufs)
@@ -298,7 +321,7 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
 def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
                 lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0,
                 comm_priority=3, n_iter=10, reps=20, warmup=10, flags=0, timeline=None,
-                wg_trace=None, comm_rate_gbs=0.0):
+                wg_trace=None, comm_rate_gbs=0.0, b_layout="nk"):
     """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
 
     Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
@@ -306,11 +329,12 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
     tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
     optional int32 GPU tensor of 4 + 12*cap entries (see occ_overlap_cfg.wg_trace).
     ``comm_rate_gbs``: bandwidth pacing of the collective in the overlapped
-    schedule (0 = full speed).  Returns the occ_overlap_result fields as a dict.
+    schedule (0 = full speed).  ``b_layout``: "nk" (B is N x K, C = A B^T) or
+    "kn" (B is K x N, C = A B).  Returns the occ_overlap_result fields as a dict.
     """
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
                           gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup,
-                          flags, timeline, wg_trace, comm_rate_gbs)
+                          flags, timeline, wg_trace, comm_rate_gbs, b_layout)
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}

@@ -21,8 +21,9 @@ DeviceInfo g_info[kMaxDevices];
 
 }  // namespace
 
-int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K) {
+int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K, bool b_kn) {
   if (M < 0 || N < 0 || K < 0 || K % 8 != 0) return OCC_EINVAL;
+  if (b_kn && N % 8 != 0) return OCC_EINVAL;  // 16-byte rows of a K x N B
   if (M == 0 || N == 0) return OCC_OK;
   if (C == nullptr || !aligned(C, 16)) return OCC_EINVAL;
   if (K > 0 && (A == nullptr || B == nullptr || !aligned(A, 16) || !aligned(B, 16))) return OCC_EINVAL;
@@ -107,11 +108,26 @@ int occ_gemm(const void *A, const void *B, void *C, int M, int N, int K, size_t 
   return occ_gemm_ex(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream);
 }
 
+int occ_gemm_kn_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                   int variant, int grid_cap, void *stream) {
+  int st = occ::validate_gemm(A, B, C, M, N, K, true);
+  if (st != OCC_OK) return st;
+  if (grid_cap < 0 || variant < 0) return OCC_EINVAL;
+  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}, true};
+  return occ::gemm_launch(c, static_cast<hipStream_t>(stream));
+}
+
+int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                void *stream) {
+  return occ_gemm_kn_ex(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream);
+}
+
 int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                         occ_gemm_plan *plan) {
   if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
   memset(plan, 0, sizeof *plan);
-  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}};
+  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0},
+                  occ::gemm_variant_is_kn(variant)};
   return occ::gemm_plan(c, plan);
 }
 

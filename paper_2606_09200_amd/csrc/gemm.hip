@@ -37,11 +37,13 @@ struct Variant {
   const char *name;
   int kmax;          // largest K the kernel takes (0 = any)
   int kmult;         // K must be a multiple of this (0 = any)
+  bool b_kn;         // takes B stored K x N (and only that)
+  int nmax;          // largest N the kernel takes (0 = any)
 };
 
 template <class T>
 constexpr Variant make_variant(int id, const char *name) {
-  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name, 0, 0};
+  return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name, 0, 0, false, 0};
 }
 
 // The direct-to-LDS kernel addresses a load pass with 32-bit byte offsets
@@ -51,23 +53,29 @@ constexpr int dl_kmax() {
   return (int)(((0xFFFFFFFFull / 2) / (unsigned long long)(T::ROWS_PER_PASS + 1)) & ~7ull);
 }
 
+// A K x N B pass is addressed the same way with N in place of K.
+template <class T>
+constexpr int dl_nmax() {
+  return T::BKN ? (int)(((0xFFFFFFFFull / 2) / (unsigned long long)(T::B_RPP + 1)) & ~7ull) : 0;
+}
+
 template <class T>
 constexpr Variant make_dl_variant(int id, const char *name) {
   return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_dl_kernel<T>, nullptr, name,
-                 dl_kmax<T>(), 0};
+                 dl_kmax<T>(), 0, T::BKN, dl_nmax<T>()};
 }
 
 template <int WAVES, int UNROLL>
 constexpr Variant make_skinny_variant(int id, const char *name) {
   return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, (WAVES - 1) * 64 * 16, nullptr,
-                 gemm_skinny_kernel<WAVES, UNROLL>, name, 0, 0};
+                 gemm_skinny_kernel<WAVES, UNROLL>, name, 0, 0, false, 0};
 }
 
 template <int WAVES, int KBW, int UNROLL>
 constexpr Variant make_skinny_areg_variant(int id, const char *name) {
   return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, 2 * (WAVES - 1) * 64 * 16, nullptr,
                  gemm_skinny_areg_kernel<WAVES, KBW, UNROLL>, name, WAVES * KBW * kSkinnyKB,
-                 2 * WAVES * kSkinnyKB * UNROLL};
+                 2 * WAVES * kSkinnyKB * UNROLL, false, 0};
 }
 
 using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
@@ -94,6 +102,9 @@ using P256x128k32_4w_2s = Tile<256, 128, 32, 2, 2, 2, true, 2>;
 using P128x256k32_4w_2s = Tile<128, 256, 32, 1, 4, 2, true, 2>;
 using P256x128k32_4w_3s = Tile<256, 128, 32, 2, 2, 3, true, 2>;
 using P128x256k32_4w_3s = Tile<128, 256, 32, 1, 4, 3, true, 2>;
+
+// B stored K x N (transpose reads from LDS)
+using PKN256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true, 1, true>;
 
 constexpr int kSkinnyId = 8;
 
@@ -127,11 +138,14 @@ const Variant kVariants[] = {
     make_dl_variant<P128x256k32_4w_3s>(27, "dl+pipe 128x256x32 4w 3st"),
     make_skinny_areg_variant<8, 32, 4>(28, "skinny M<=16, A in registers, 8 waves, K<=8192, K%2048==0"),
     make_skinny_areg_variant<8, 16, 4>(29, "skinny M<=16, A in registers, 8 waves, K<=4096, K%2048==0"),
+    make_dl_variant<PKN256x256_8w_2s>(32, "dl+pipe 256x256x64 8w 2st, B K x N"),
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
+
+constexpr int kKnVariant = 32;  // the K x N B kernel
 
 const Variant *find_variant(int id) {
   for (const Variant &v : kVariants)
@@ -158,6 +172,11 @@ int auto_variant(int M, int N, int K, int num_cus) {
 
 }  // namespace
 
+bool gemm_variant_is_kn(int id) {
+  const Variant *v = find_variant(id);
+  return v != nullptr && v->b_kn;
+}
+
 static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_gemm_plan *p) {
   const Variant *v = find_variant(variant);
   if (v == nullptr) return OCC_EINVAL;
@@ -165,6 +184,8 @@ static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_g
   if (skinny && c.M > 16) return OCC_EINVAL;
   if (v->kmax > 0 && c.K > v->kmax) return OCC_EINVAL;
   if (v->kmult > 0 && (c.K == 0 || c.K % v->kmult != 0)) return OCC_EINVAL;
+  if (v->b_kn != c.b_kn) return OCC_EINVAL;  // the variant reads B in the other layout
+  if (v->nmax > 0 && c.N > v->nmax) return OCC_EINVAL;
   if (v->id < 0 || v->id > kMaxVariantId) return OCC_EINVAL;
   p->tile_m = v->bm;
   p->tile_n = v->bn;
@@ -191,7 +212,7 @@ int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
   int st = current_device_info(&di);
   if (st != OCC_OK) return st;
   int variant = c.variant;
-  if (variant == 0) variant = auto_variant(c.M, c.N, c.K, di->num_cus);
+  if (variant == 0) variant = c.b_kn ? kKnVariant : auto_variant(c.M, c.N, c.K, di->num_cus);
   st = fill_plan(c, variant, *di, plan);
   if (st != OCC_OK) return st;
   const Variant *v = find_variant(variant);

@@ -23,25 +23,35 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 // so that the 32 rows of an MFMA operand read hit distinct banks), with the
 // next k-step's global loads in flight in registers while the current one is
 // multiplied.  STAGES = 2 double-buffers the LDS (one barrier per k-step).
-template <int BM_, int BN_, int BK_, int WM_, int WN_, int STAGES_, bool PIPE_ = false, int MINB_ = 1>
+template <int BM_, int BN_, int BK_, int WM_, int WN_, int STAGES_, bool PIPE_ = false, int MINB_ = 1,
+          bool BKN_ = false>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_, STAGES = STAGES_;
   static constexpr bool PIPE = PIPE_;  // enforce LDS-read / MFMA interleaving
   static constexpr int MINB = MINB_;   // workgroups per CU the register budget must allow
+  // B stored K x N (N-contiguous) instead of N x K: its LDS tile is BK rows of
+  // BN columns and MFMA fragments are read with LDS transpose reads
+  // (direct-to-LDS kernel only)
+  static constexpr bool BKN = BKN_;
   static constexpr int NT = 64 * WM * WN;
   static constexpr int TM = BM / WM, TN = BN / WN;
   static constexpr int FM = TM / 32, FN = TN / 32;
   static constexpr int KCH = BK / 8;              // 16-byte chunks per tile row
   static constexpr int ROWS_PER_PASS = NT / KCH;  // rows the workgroup loads per pass
+  static constexpr int BCH = BN / 8;              // 16-byte chunks per K x N B row
+  static constexpr int B_RPP = BKN ? NT / BCH : ROWS_PER_PASS;  // B rows per pass
+  static constexpr int BROW_BYTES = BN * 2;       // K x N B row in LDS
   static constexpr int A_LOADS = BM / ROWS_PER_PASS;
-  static constexpr int B_LOADS = BN / ROWS_PER_PASS;
+  static constexpr int B_LOADS = BKN ? BK / B_RPP : BN / ROWS_PER_PASS;
   static constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = A_BYTES + B_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be whole 32x32 blocks");
   static_assert(KCH == 4 || KCH == 8, "BK must be 32 or 64");
   static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small for the workgroup");
-  static_assert(BM % ROWS_PER_PASS == 0 && BN % ROWS_PER_PASS == 0, "uneven load passes");
+  static_assert(BM % ROWS_PER_PASS == 0, "uneven load passes");
+  static_assert(BKN ? (BK % B_RPP == 0 && B_RPP % 4 == 0 && BCH >= 16) : (BN % ROWS_PER_PASS == 0),
+                "uneven load passes");
 };
 
 // Physical 16-byte chunk of logical chunk c in tile row r.  The LDS has 64
@@ -56,6 +66,14 @@ __device__ __forceinline__ int swz(int r, int c) {
   if constexpr (KCH == 8) return c ^ ((r >> 1) & 7);
   else return c ^ ((r >> 2) & 3);
 }
+
+// Physical 16-byte chunk of logical chunk c in row k of a K x N B tile.  A
+// transpose read sends, per 16 lanes, 4 consecutive rows at one 32-byte
+// column piece (per 32 lanes: 4 rows x 64 bytes); rows are BN*2 bytes, a
+// multiple of 256, so all 4 rows would hit the same banks.  XOR-ing the chunk
+// with 4*(k % 4) moves the 4 rows' 64-byte pieces to 4 different 64-byte
+// quarters of the bank line.
+__device__ __forceinline__ int swz_kn(int k, int c) { return c ^ ((k & 3) << 2); }
 
 // XCD-aware order: dispatch hands consecutive workgroups to the 8 XCDs in
 // turn, so tile ids are regrouped to give each XCD a contiguous run of the

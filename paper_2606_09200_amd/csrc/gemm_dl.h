@@ -16,6 +16,7 @@ namespace {
 // M (N) lie beyond the tile panel's num_records, and chunks past K get an
 // offset beyond any panel.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ i32x4 make_rsrc(const void *base, uint32_t bytes) {
   const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -92,6 +93,17 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
   const int c = q ^ (swz<T::KCH>(r_in, 0));
   const uint32_t lane_off = (uint32_t)r_in * (uint32_t)K * 2u + (uint32_t)c * 16u;
   const uint32_t wave_lds = (uint32_t)wave * 1024u;
+  // K x N B: this lane's slot in every B pass, row rB of the pass and
+  // physical chunk qB; passes start at multiples of 4 rows, so the logical
+  // chunk qB ^ swz is the same in every pass.
+  const int rB = threadIdx.x / T::BCH;
+  const int cB = swz_kn(rB, threadIdx.x % T::BCH);
+  // K x N B fragment reads (transpose reads, see below): within each group of
+  // 16 lanes, lane s reads 4 consecutive columns at row (s / 4) of a 4-row
+  // block; the hardware hands lane i of the group element j of lane
+  // 4 * j + i / 4, i.e. 4 consecutive k of column i.
+  const int tr_k = 8 * ((lane >> 4) >> 1) + ((lane & 15) >> 2);
+  const int tr_n = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
     int tm, tn;
@@ -103,6 +115,11 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
       const int have = min(T::ROWS_PER_PASS, max(0, rows - row0));
       return make_rsrc(base + (size_t)row0 * K, (uint32_t)have * (uint32_t)K * 2u);
     };
+    // K x N B: columns past N read as zero through an out-of-range offset,
+    // rows past K through each pass's num_records
+    const uint32_t vb = (n0 + cB * 8 < N) ? (uint32_t)rB * (uint32_t)N * 2u + (uint32_t)(n0 + cB * 8) * 2u
+                                          : 0x80000000u;
+    (void)vb;
     auto issue = [&](int kt) {
       const int k0 = kt * T::BK;
       const uint32_t sbase = lds0 + (uint32_t)((kt % S) * T::STAGE_BYTES) + wave_lds;
@@ -110,10 +127,20 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
 #pragma unroll
       for (int p = 0; p < T::A_LOADS; ++p)
         lds_dma16(pass_rsrc(A, m0 + p * T::ROWS_PER_PASS, M), sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), v);
+      if constexpr (T::BKN) {
 #pragma unroll
-      for (int p = 0; p < T::B_LOADS; ++p)
-        lds_dma16(pass_rsrc(B, n0 + p * T::ROWS_PER_PASS, N),
-                  sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES), v);
+        for (int p = 0; p < T::B_LOADS; ++p) {
+          const int kr0 = k0 + p * T::B_RPP;
+          const int have = min(T::B_RPP, max(0, K - kr0));
+          lds_dma16(make_rsrc(B + (size_t)kr0 * N, (uint32_t)have * (uint32_t)N * 2u),
+                    sbase + (uint32_t)(T::A_BYTES + p * T::B_RPP * T::BROW_BYTES), vb);
+        }
+      } else {
+#pragma unroll
+        for (int p = 0; p < T::B_LOADS; ++p)
+          lds_dma16(pass_rsrc(B, n0 + p * T::ROWS_PER_PASS, N),
+                    sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES), v);
+      }
     };
 
     f32x16 acc[T::FM][T::FN];
@@ -154,11 +181,25 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
               bf16x8, *reinterpret_cast<const u32x4 *>(cur + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
         }
         const unsigned char *bs = cur + T::A_BYTES;
+        if constexpr (T::BKN) {
+          const int kr = ks * 16 + tr_k;
 #pragma unroll
-        for (int j = 0; j < T::FN; ++j) {
-          int r = brow + j * 32;
-          fb[j] = __builtin_bit_cast(
-              bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
+          for (int j = 0; j < T::FN; ++j) {
+            const int n = wn * T::TN + j * 32 + tr_n;
+            const int off = swz_kn(kr, n >> 3) * 16 + (n & 7) * 2;
+            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) i16x4 *)(bs + kr * T::BROW_BYTES + off));
+            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) i16x4 *)(bs + (kr + 4) * T::BROW_BYTES + off));
+            fb[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < T::FN; ++j) {
+            int r = brow + j * 32;
+            fb[j] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
+          }
         }
       };
       load_frags(0, af[0], bfr[0]);
@@ -172,7 +213,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][i], bfr[ks & 1][j], acc[i][j], 0, 0, 0);
       }
       if constexpr (T::PIPE) {
-        constexpr int NF = T::FM + T::FN;      // LDS reads per substep
+        constexpr int NF = T::FM + (T::BKN ? 2 : 1) * T::FN;  // LDS reads per substep
         constexpr int NMF = T::FM * T::FN;     // MFMAs per substep
         __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
 #pragma unroll

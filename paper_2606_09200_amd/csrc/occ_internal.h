@@ -36,8 +36,10 @@ struct GemmCall {
   int variant;          // 0 = automatic, else a kernel variant id
   int priority;         // wave priority 0..3 (s_setprio)
   KTrace trace;         // optional tracing (all null = off)
+  bool b_kn = false;    // B stored K x N (C = A B) instead of N x K (C = A B^T)
 };
 int gemm_plan(const GemmCall &c, occ_gemm_plan *plan);
+bool gemm_variant_is_kn(int id);  // a variant that takes B stored K x N
 int gemm_launch(const GemmCall &c, hipStream_t s);
 
 // ---- communication-side kernels -----------------------------------------
@@ -69,7 +71,7 @@ int permute_launch(const PermuteCall &c, hipStream_t s);
 int permute_default_wgs(const PermuteCall &c);
 
 // ---- validation (host only, no HIP calls) --------------------------------
-int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K);
+int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K, bool b_kn = false);
 int validate_reduce(const float *const *bufs, int nchunks, size_t len, const float *out);
 int validate_permute(const void *src, const void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes);

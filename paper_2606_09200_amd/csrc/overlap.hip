@@ -107,7 +107,8 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
   if (!(c->comm_rate_gbs == 0.0 || (c->comm_rate_gbs >= OCC_MIN_COMM_RATE_GBS && c->comm_rate_gbs <= 1.0e6)))
     return OCC_EINVAL;
-  OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K));
+  if (c->gemm_b_layout != 0 && c->gemm_b_layout != 1) return OCC_EINVAL;
+  OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K, c->gemm_b_layout == 1));
   size_t cbytes = (size_t)c->M * c->N * 2;
   // K_g writes C while K_c runs: C must not overlap anything K_c touches,
   // and K_c's output must not overlap A or B.
@@ -211,7 +212,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   L.kind = c.comm_kind;
   const KTrace off{nullptr, nullptr, 0, 0};
   L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
-                 c.gemm_priority, off};
+                 c.gemm_priority, off, c.gemm_b_layout == 1};
   L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
   L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
   L.rate_gbs = c.comm_rate_gbs;
@@ -377,7 +378,7 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   int npads = 1;
   {
     GemmCall g{cfg->A, cfg->B, cfg->C, cfg->M, cfg->N, cfg->K, 0, 0, cfg->gemm_variant,
-               cfg->gemm_priority, KTrace{nullptr, nullptr, 0, 0}};
+               cfg->gemm_priority, KTrace{nullptr, nullptr, 0, 0}, cfg->gemm_b_layout == 1};
     occ_gemm_plan p0;
     OCC_TRY(gemm_plan(g, &p0));
     if (p0.wg_per_cu > 1) {

@@ -39,9 +39,9 @@ def test_strerror_and_version(L):
     for code in range(0, -7, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == binding.ABI_VERSION == (1, 1)
+    assert binding.occ_version() == binding.ABI_VERSION == (1, 2)
     hdr = open(HEADER).read()
-    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 1" in hdr
+    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 2" in hdr
 
 
 P = ctypes.c_void_p
@@ -56,6 +56,18 @@ def test_gemm_argument_errors(L):
     assert L.occ_gemm(P(0x1000), P(0x2000), P(0x1010), 4, 4, 8, 0, None) == -4  # C inside A
     assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, -1, 0, None) == -1
     assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, 0, -5, None) == -1
+
+
+def test_gemm_kn_argument_errors(L):
+    # K x N B: 16-byte rows need N % 8 == 0, on top of occ_gemm's checks
+    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None) == -1
+    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x3000), 4, 8, 12, 0, None) == -1
+    assert L.occ_gemm_kn(P(0x1000), None, P(0x3000), 4, 8, 8, 0, None) == -1
+    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x2010), 4, 8, 8, 0, None) == -4  # C inside B
+    assert L.occ_gemm_kn_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, -1, 0, None) == -1
+    assert L.occ_gemm_kn_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, 0, -1, None) == -1
+    # N % 8 != 0 is fine for the N x K layout (fails later, with no device)
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None) != -1
 
 
 def test_reduce_argument_errors(L):
@@ -119,6 +131,13 @@ def test_run_overlap_argument_errors(L):
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1
     cfg.flags = 0
     cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    cfg.gemm_b_layout = 2                                                 # neither N x K nor K x N
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.gemm_b_layout, cfg.N = 1, 12                                      # K x N needs N % 8 == 0
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.N = 8
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1
+    cfg.gemm_b_layout = 0
     for rate in (-1.0, 5.0, float("nan"), 1e7):                          # pacing out of range
         cfg.comm_rate_gbs = rate
         assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1, rate

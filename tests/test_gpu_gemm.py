@@ -208,3 +208,89 @@ def test_gemm_full_size_skinny_full_parity():
         occ.occ_gemm_ex(A, B, C, variant=v)
         torch.cuda.synchronize()
         assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full, variant %d" % v)
+
+
+# ------------------------------------------------------------- B stored K x N
+def run_gemm_kn(A, Bkn, lds_bytes=0, variant=0, grid_cap=0):
+    M, K = A.shape
+    N = Bkn.shape[1]
+    Ad, Bd = A.to(DEV), Bkn.to(DEV)
+    C = torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm_kn_ex(Ad, Bd, C, lds_bytes=lds_bytes, variant=variant, grid_cap=grid_cap)
+    torch.cuda.synchronize()
+    return bf16_bits(C)
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 512, 512), (300, 264, 136), (1, 8, 8), (17, 40, 64),
+                                   (257, 136, 520), (64, 64, 32), (520, 1000, 1032),
+                                   (16, 256, 4096), (600, 776, 200)])
+def test_gemm_kn_full_parity(M, N, K):
+    A, B = inputs.gemm_operands(M, N, K, seed=4)
+    Bkn = B.t().contiguous()
+    got = run_gemm_kn(A, Bkn)
+    ref = oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn")
+    assert_gemm_close(got, ref, 1.0, 1.0, K, "kn %dx%dx%d" % (M, N, K))
+    # the same tile, MFMA sequence and k order as the N x K kernel: same bits
+    assert np.array_equal(got, run_gemm(A, B, variant=16))
+
+
+def test_gemm_kn_integer_bit_exact_and_invariant():
+    A, B = int_operands(333, 272, 712, seed=9)
+    Bkn = B.t().contiguous()
+    base = run_gemm_kn(A, Bkn)
+    assert np.array_equal(base, oracle.gemm_bf16(A, Bkn, 333, 272, 712, b_layout="kn"))
+    for cap in (1, 3, 256):
+        assert np.array_equal(run_gemm_kn(A, Bkn, grid_cap=cap), base), cap
+    assert np.array_equal(run_gemm_kn(A, Bkn, lds_bytes=16 << 10, variant=32), base)
+
+
+def test_gemm_kn_layout_checks():
+    A, B = inputs.gemm_operands(64, 12, 64, seed=1, device=DEV)
+    Bkn = B.t().contiguous()
+    C = torch.empty((64, 12), device=DEV, dtype=torch.bfloat16)
+    with pytest.raises(occ.OccError) as e:            # N % 8 != 0
+        occ.occ_gemm_kn(A, Bkn, C)
+    assert e.value.status == occ.OCC_EINVAL
+    A, B = inputs.gemm_operands(64, 16, 64, seed=1, device=DEV)
+    Bkn = B.t().contiguous()
+    C = torch.empty((64, 16), device=DEV, dtype=torch.bfloat16)
+    for v in (1, 16, 21):                               # variants that read B as N x K
+        with pytest.raises(occ.OccError) as e:
+            occ.occ_gemm_kn_ex(A, Bkn, C, variant=v)
+        assert e.value.status == occ.OCC_EINVAL, v
+    with pytest.raises(occ.OccError) as e:              # and the reverse
+        occ.occ_gemm_ex(A, B, C, variant=32)
+    assert e.value.status == occ.OCC_EINVAL
+    p = occ.occ_gemm_plan_query(8192, 8192, 8192, 0, 32)
+    q = occ.occ_gemm_plan_query(8192, 8192, 8192, 0, 16)
+    assert p["kernel_id"] == 32 and p["tile_lds_bytes"] == q["tile_lds_bytes"]
+    assert (p["tile_m"], p["tile_n"], p["tile_k"], p["grid"]) == (q["tile_m"], q["tile_n"], q["tile_k"], q["grid"])
+    assert p["wg_per_cu"] >= 1
+
+
+def test_gemm_kn_zero_k_and_empty():
+    C = torch.full((20, 32), 1.0, device=DEV, dtype=torch.bfloat16)
+    Ad = torch.zeros((20, 8), dtype=torch.bfloat16, device=DEV)[:, :0]
+    occ.lib().occ_gemm_kn(occ._ptr(Ad), None, occ._ptr(C), 20, 32, 0, 0, occ._stream(None))
+    torch.cuda.synchronize()
+    assert np.all(bf16_bits(C) == 0)
+    A = torch.zeros((0, 64), dtype=torch.bfloat16)
+    assert run_gemm_kn(A, torch.zeros((64, 16), dtype=torch.bfloat16)).shape == (0, 16)
+
+
+def test_gemm_kn_full_size_sampled_and_equal_to_nk():
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS["cb"]
+    A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, device=DEV)
+    Bkn = B.t().contiguous()
+    C = torch.empty((w.M, w.N), device=DEV, dtype=torch.bfloat16)
+    C_nk = torch.empty_like(C)
+    occ.occ_gemm_kn(A, Bkn, C)
+    occ.occ_gemm_ex(A, B, C_nk, variant=16)
+    torch.cuda.synchronize()
+    assert torch.equal(C.view(torch.int16), C_nk.view(torch.int16))
+    Ah, Bh, Ch = bf16_bits(A), bf16_bits(Bkn), bf16_bits(C)
+    for m0, n0 in sample_tiles(w.M, w.N, count=12):
+        m1, n1 = min(m0 + 64, w.M), min(n0 + 64, w.N)
+        ref = oracle.gemm_bf16(Ah, Bh, w.M, w.N, w.K, b_layout="kn", rows=(m0, m1), cols=(n0, n1))
+        assert_gemm_close(Ch[m0:m1, n0:n1], ref, 1.0, 1.0, w.K, "cb kn tile %d,%d" % (m0, n0))

@@ -244,3 +244,21 @@ def test_pace_all_paces_every_schedule():
     assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
     assert r["t_comm_ms"] >= 0.8 * paced_ms, r
     assert r["t_seq_ms"] >= 0.8 * 2 * paced_ms and r["t_ovl_ms"] >= 0.8 * 2 * paced_ms, r
+
+
+def test_overlap_with_kn_b_matches_plain_calls():
+    A, B, C, chunks, out = tiny_reduce_setup(M=520, N=264, K=200)
+    Bkn = B.t().contiguous()
+    C_ref = torch.empty_like(C)
+    occ.occ_gemm_kn(A, Bkn, C_ref)
+    torch.cuda.synchronize()
+    r = occ.run_overlap(A, Bkn, C, bufs=chunks, out=out, b_layout="kn", comm_priority=0,
+                        n_iter=3, reps=2, warmup=1)
+    torch.cuda.synchronize()
+    assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
+    assert r["t_seq_ms"] > 0 and r["t_ovl_ms"] > 0
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(Bkn), 520, 264, 200, b_layout="kn")
+    assert_gemm_close(bf16_bits(C), ref, 1.0, 1.0, 200, "overlap kn C")
+    with pytest.raises(occ.OccError):                   # a variant that reads N x K
+        occ.run_overlap(A, Bkn, C, bufs=chunks, out=out, b_layout="kn", gemm_variant=16,
+                        n_iter=1, reps=1, warmup=0)
