@@ -120,9 +120,10 @@ enum {
  * results; the skinny variants (8, 20-23, 28, 29) split K across waves and
  * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
  * an unknown variant, a skinny variant with M > 16, a K that variant 28/29
- * does not take, or K above 16 M (the direct-to-LDS variants 10-19, 24-27
- * address a load pass with 32-bit offsets; for such K the automatic choice
- * falls back to a register-staged variant).
+ * does not take, or K above 4 M for a direct-to-LDS variant with 256-row
+ * tiles (8 M with 128-row tiles: variants 10-19, 24-27, 32-38 address an
+ * operand tile with 32-bit offsets; for such K the automatic choice falls
+ * back to a register-staged variant).
  */
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);
@@ -133,9 +134,9 @@ int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size
  * as occ_gemm; the B tile is staged in LDS as stored and its MFMA operands
  * are read with gfx950's LDS transpose reads.  Results are bit-identical to
  * occ_gemm on the transposed B (same order of the k sums).
- * Requirements: as occ_gemm, plus N % 8 == 0 (16-byte B rows) and N at
- * most about 1.26e8 (a 16-row load pass of B is addressed with 32-bit
- * offsets; larger N is OCC_EINVAL).
+ * Requirements: as occ_gemm, plus N % 8 == 0 (16-byte B rows), N at most
+ * 16 M and K at most 4 M (a k-step of B and a tile of A are addressed with
+ * 32-bit offsets; larger is OCC_EINVAL).
  */
 int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 void *stream);

@@ -46,17 +46,19 @@ constexpr Variant make_variant(int id, const char *name) {
   return Variant{id, T::BM, T::BN, T::BK, T::NT, T::LDS_BYTES, gemm_tiled_kernel<T>, nullptr, name, 0, 0, false, 0};
 }
 
-// The direct-to-LDS kernel addresses a load pass with 32-bit byte offsets
-// (row within the pass * K * 2 + k * 2): K is capped so that they cannot wrap.
+// The direct-to-LDS kernel addresses an operand tile with 32-bit byte
+// offsets from the tile's first row (row * K * 2 + k * 2) and marks missing
+// k with an offset of 2^31: K is capped so that a tile spans at most 2^31
+// bytes (no offset wraps and every marked offset is out of range).
 template <class T>
 constexpr int dl_kmax() {
-  return (int)(((0xFFFFFFFFull / 2) / (unsigned long long)(T::ROWS_PER_PASS + 1)) & ~7ull);
+  return (int)((0x80000000ull / (2ull * (unsigned long long)(T::BM > T::BN ? T::BM : T::BN))) & ~7ull);
 }
 
-// A K x N B pass is addressed the same way with N in place of K.
+// A K x N B k-step (BK rows of N) is addressed the same way with N in place of K.
 template <class T>
 constexpr int dl_nmax() {
-  return T::BKN ? (int)(((0xFFFFFFFFull / 2) / (unsigned long long)(T::B_RPP + 1)) & ~7ull) : 0;
+  return T::BKN ? (int)((0x80000000ull / (2ull * (unsigned long long)T::BK)) & ~7ull) : 0;
 }
 
 template <class T>

@@ -84,15 +84,18 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
   const uint32_t lds0 = (uint32_t)(size_t)(__attribute__((address_space(3))) unsigned char *)smem;
 
   // This lane's slot in every load pass: row r_in of the pass, physical
-  // chunk q; the swizzle is the same for all passes of a lane, so one offset
-  // (plus k0) serves every pass: each pass gets a buffer descriptor of its
-  // own, based at the pass's first row, whose num_records covers only the
-  // pass's rows that exist.
+  // chunk q; the swizzle is the same for all passes of a lane.  Each operand
+  // tile is read through one buffer descriptor based at the tile's first row
+  // whose num_records covers only the rows that exist; pass p adds
+  // p * ROWS_PER_PASS rows to the lane's offset (a VALU add against a uniform
+  // step, so that issuing a pass needs no scalar work that waits on vector
+  // results).  Offsets stay below 2^31 (the variant's K limit).
   const int r_in = threadIdx.x / T::KCH;
   const int q = threadIdx.x % T::KCH;
   const int c = q ^ (swz<T::KCH>(r_in, 0));
   const uint32_t lane_off = (uint32_t)r_in * (uint32_t)K * 2u + (uint32_t)c * 16u;
-  const uint32_t wave_lds = (uint32_t)wave * 1024u;
+  const uint32_t pass_step = (uint32_t)T::ROWS_PER_PASS * (uint32_t)K * 2u;
+  const uint32_t wave_lds = (uint32_t)__builtin_amdgcn_readfirstlane(wave) * 1024u;
   // K x N B: this lane's slot in every B pass, row rB of the pass and
   // physical chunk qB; passes start at multiples of 4 rows, so the logical
   // chunk qB ^ swz is the same in every pass.
@@ -111,36 +114,36 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
     const int m0 = tm * T::BM;
     const int n0 = tn * T::BN;
 
-    auto pass_rsrc = [&](const uint16_t *base, int row0, int rows) {
-      const int have = min(T::ROWS_PER_PASS, max(0, rows - row0));
-      return make_rsrc(base + (size_t)row0 * K, (uint32_t)have * (uint32_t)K * 2u);
-    };
+    const i32x4 rsrc_a = make_rsrc(A + (size_t)m0 * K, (uint32_t)min(T::BM, M - m0) * (uint32_t)K * 2u);
+    const i32x4 rsrc_b = T::BKN ? rsrc_a : make_rsrc(B + (size_t)n0 * K, (uint32_t)min(T::BN, N - n0) * (uint32_t)K * 2u);
     // K x N B: columns past N read as zero through an out-of-range offset,
-    // rows past K through each pass's num_records
+    // rows past K through the k-step's num_records
     const uint32_t vb = (n0 + cB * 8 < N) ? (uint32_t)rB * (uint32_t)N * 2u + (uint32_t)(n0 + cB * 8) * 2u
                                           : 0x80000000u;
     (void)vb;
-    auto issue = [&](int kt) {
+    // DMA pass p of k-step kt: A passes first, then B passes.  A k-step past
+    // K loads nothing and writes zeros (every offset is out of range).
+    auto issue_pass = [&](int kt, int p) {
       const int k0 = kt * T::BK;
       const uint32_t sbase = lds0 + (uint32_t)((kt % S) * T::STAGE_BYTES) + wave_lds;
       const uint32_t v = (k0 + c * 8 < K) ? lane_off + (uint32_t)k0 * 2u : 0x80000000u;
-#pragma unroll
-      for (int p = 0; p < T::A_LOADS; ++p)
-        lds_dma16(pass_rsrc(A, m0 + p * T::ROWS_PER_PASS, M), sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), v);
-      if constexpr (T::BKN) {
-#pragma unroll
-        for (int p = 0; p < T::B_LOADS; ++p) {
-          const int kr0 = k0 + p * T::B_RPP;
-          const int have = min(T::B_RPP, max(0, K - kr0));
-          lds_dma16(make_rsrc(B + (size_t)kr0 * N, (uint32_t)have * (uint32_t)N * 2u),
-                    sbase + (uint32_t)(T::A_BYTES + p * T::B_RPP * T::BROW_BYTES), vb);
-        }
+      if (p < T::A_LOADS) {
+        lds_dma16(rsrc_a, sbase + (uint32_t)(p * T::ROWS_PER_PASS * ROW_BYTES), v + (uint32_t)p * pass_step);
+      } else if constexpr (T::BKN) {
+        const int q = p - T::A_LOADS;
+        const int have = min(T::BK, max(0, K - k0));
+        lds_dma16(make_rsrc(B + (size_t)k0 * N, (uint32_t)have * (uint32_t)N * 2u),
+                  sbase + (uint32_t)(T::A_BYTES + q * T::B_RPP * T::BROW_BYTES),
+                  vb + (uint32_t)(q * T::B_RPP) * (uint32_t)N * 2u);
       } else {
-#pragma unroll
-        for (int p = 0; p < T::B_LOADS; ++p)
-          lds_dma16(pass_rsrc(B, n0 + p * T::ROWS_PER_PASS, N),
-                    sbase + (uint32_t)(T::A_BYTES + p * T::ROWS_PER_PASS * ROW_BYTES), v);
+        const int q = p - T::A_LOADS;
+        lds_dma16(rsrc_b, sbase + (uint32_t)(T::A_BYTES + q * T::ROWS_PER_PASS * ROW_BYTES),
+                  v + (uint32_t)q * pass_step);
       }
+    };
+    auto issue = [&](int kt) {
+#pragma unroll
+      for (int p = 0; p < PER_STAGE; ++p) issue_pass(kt, p);
     };
 
     f32x16 acc[T::FM][T::FN];
@@ -159,6 +162,43 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
     const int brow = wn * T::TN + (lane & 31);
     const int half = lane >> 5;
 
+    // MFMA operand fragments of 16-wide k-substep ks of the stage at `cur`
+    auto read_a = [&](const unsigned char *cur, int ks, int i) {
+      const int r = arow + i * 32;
+      return __builtin_bit_cast(
+          bf16x8, *reinterpret_cast<const u32x4 *>(cur + r * ROW_BYTES + swz<T::KCH>(r, ks * 2 + half) * 16));
+    };
+    auto read_b = [&](const unsigned char *cur, int ks, int j) {
+      const unsigned char *bs = cur + T::A_BYTES;
+      if constexpr (T::BKN) {
+        const int kr = ks * 16 + tr_k;
+        const int n = wn * T::TN + j * 32 + tr_n;
+        const int off = swz_kn(kr, n >> 3) * 16 + (n & 7) * 2;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4 *)(bs + kr * T::BROW_BYTES + off));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) i16x4 *)(bs + (kr + 4) * T::BROW_BYTES + off));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        const int r = brow + j * 32;
+        return __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * ROW_BYTES + swz<T::KCH>(r, ks * 2 + half) * 16));
+      }
+    };
+    constexpr int KS = T::BK / 16;
+    constexpr int NF = T::FM + (T::BKN ? 2 : 1) * T::FN;  // LDS reads per substep
+    constexpr int NMF = T::FM * T::FN;                     // MFMAs per substep
+    bf16x8 af[2][T::FM], bfr[2][T::FN];
+    auto load_frags = [&](const unsigned char *cur, int ks, int set) {
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i) af[set][i] = read_a(cur, ks, i);
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j) bfr[set][j] = read_b(cur, ks, j);
+    };
+    auto mfma = [&](int x, int set) {
+      const int i = x / T::FN, j = x % T::FN;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[set][i], bfr[set][j], acc[i][j], 0, 0, 0);
+    };
     for (int kt = 0; kt < nk; ++kt) {
       // k-step kt has landed once at most min(S-2, nk-1-kt) later steps are
       // outstanding; the barrier then publishes it and retires step kt-1.
@@ -170,65 +210,25 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
       // of substep ks run (two register sets); the scheduling groups below
       // interleave one LDS read after each MFMA.
       const unsigned char *cur = smem + (kt % S) * T::STAGE_BYTES;
-      constexpr int KS = T::BK / 16;
-      bf16x8 af[2][T::FM], bfr[2][T::FN];
-      auto load_frags = [&](int ks, bf16x8(&fa)[T::FM], bf16x8(&fb)[T::FN]) {
-        const int cc = ks * 2 + half;
-#pragma unroll
-        for (int i = 0; i < T::FM; ++i) {
-          int r = arow + i * 32;
-          fa[i] = __builtin_bit_cast(
-              bf16x8, *reinterpret_cast<const u32x4 *>(cur + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
-        }
-        const unsigned char *bs = cur + T::A_BYTES;
-        if constexpr (T::BKN) {
-          const int kr = ks * 16 + tr_k;
-#pragma unroll
-          for (int j = 0; j < T::FN; ++j) {
-            const int n = wn * T::TN + j * 32 + tr_n;
-            const int off = swz_kn(kr, n >> 3) * 16 + (n & 7) * 2;
-            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) i16x4 *)(bs + kr * T::BROW_BYTES + off));
-            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                (__attribute__((address_space(3))) i16x4 *)(bs + (kr + 4) * T::BROW_BYTES + off));
-            fb[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < T::FN; ++j) {
-            int r = brow + j * 32;
-            fb[j] = __builtin_bit_cast(
-                bf16x8, *reinterpret_cast<const u32x4 *>(bs + r * ROW_BYTES + swz<T::KCH>(r, cc) * 16));
-          }
-        }
-      };
-      load_frags(0, af[0], bfr[0]);
+      load_frags(cur, 0, 0);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        if (ks + 1 < KS) load_frags(ks + 1, af[(ks + 1) & 1], bfr[(ks + 1) & 1]);
+        if (ks + 1 < KS) load_frags(cur, ks + 1, (ks + 1) & 1);
 #pragma unroll
-        for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-          for (int j = 0; j < T::FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[ks & 1][i], bfr[ks & 1][j], acc[i][j], 0, 0, 0);
+        for (int x = 0; x < NMF; ++x) mfma(x, ks & 1);
       }
       if constexpr (T::PIPE) {
-        constexpr int NF = T::FM + (T::BKN ? 2 : 1) * T::FN;  // LDS reads per substep
-        constexpr int NMF = T::FM * T::FN;     // MFMAs per substep
         __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          if (ks + 1 < KS) {
+        for (int ks = 0; ks + 1 < KS; ++ks) {
 #pragma unroll
-            for (int x = 0; x < NF; ++x) {
-              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-              __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            }
-            if constexpr (NMF > NF) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NF, 0);
-          } else {
-            __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
+          for (int x = 0; x < NF; ++x) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
+          if constexpr (NMF > NF) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NF, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
       }
     }
     __syncthreads();  // every wave is done with the stages before the next tile's prologue

@@ -23,7 +23,8 @@ from paper_2606_09200_amd.workloads import WORKLOADS  # noqa: E402
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="cb", choices=sorted(WORKLOADS))
-    ap.add_argument("--kernel", default="gemm", choices=["gemm", "comm"])
+    ap.add_argument("--kernel", default="gemm", choices=["gemm", "comm", "torch_mm"],
+                    help="torch_mm: the same GEMM through torch.mm (hipBLASLt), for comparison")
     ap.add_argument("--launches", type=int, default=5)
     ap.add_argument("--pad-kib", type=int, default=0)
     ap.add_argument("--variant", type=int, default=0)
@@ -32,10 +33,13 @@ def main(argv=None):
     a = ap.parse_args(argv)
     w = WORKLOADS[a.workload]
     dev = "cuda:0"
-    if a.kernel == "gemm":
+    if a.kernel in ("gemm", "torch_mm"):
         A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=dev)
         C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
-        run = lambda: occ.occ_gemm_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
+        if a.kernel == "gemm":
+            run = lambda: occ.occ_gemm_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
+        else:
+            run = lambda: torch.mm(A, B.t(), out=C)
     elif w.comm == "reduce":
         ch = inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev)
         out = torch.empty(w.length, device=dev)
