@@ -67,7 +67,7 @@ def make_inputs(w, dev):
     return A, B, C, comm
 
 
-def cpu_baseline(w, A, B, comm, budget_s):
+def cpu_baseline(w, A, B, comm, budget_s, b_layout="nk"):
     """The oracle, as it stands, on a bounded sample of the same step, scaled
     to one sequential pass of n_iter iterations (ms)."""
     import numpy as np
@@ -83,7 +83,7 @@ def cpu_baseline(w, A, B, comm, budget_s):
     while time.perf_counter() - t0 < budget_s / 2 and tiles < 4096:
         m0 = int(rng.integers(0, max(1, w.M - 64 + 1))) if w.M > 64 else 0
         n0 = int(rng.integers(0, max(1, w.N - 64 + 1))) if w.N > 64 else 0
-        oracle.gemm_bf16(Ah, Bh, w.M, w.N, w.K, rows=(m0, min(w.M, m0 + 64)),
+        oracle.gemm_bf16(Ah, Bh, w.M, w.N, w.K, b_layout=b_layout, rows=(m0, min(w.M, m0 + 64)),
                          cols=(n0, min(w.N, n0 + 64)))
         tiles += 1
     t_gemm_sample = time.perf_counter() - t0
@@ -126,6 +126,8 @@ def main():
     ap.add_argument("--variant", type=int, default=0, help="GEMM kernel variant (0 = auto)")
     ap.add_argument("--gemm-grid", type=int, default=0, help="persistent GEMM grid cap (0 = off)")
     ap.add_argument("--comm-wgs", type=int, default=0)
+    ap.add_argument("--b-layout", default="nk", choices=["nk", "kn"],
+                    help="GEMM B stored N x K (C = A B^T, occ_gemm) or K x N (C = A B, occ_gemm_kn)")
     ap.add_argument("--comm-rate-gbs", type=float, default=0.0,
                     help="bandwidth pacing of the collective in the overlapped schedule (0 = off)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
@@ -145,10 +147,12 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     A, B, C, comm = make_inputs(w, dev)
+    if args.b_layout == "kn":
+        B = B.t().contiguous()  # the same matrix op(B), stored K x N
     torch.cuda.synchronize()
     knobs = dict(lds_bytes=args.pad_kib << 10, gemm_variant=args.variant, gemm_grid=args.gemm_grid,
                  comm_wgs=args.comm_wgs, comm_priority=args.priority, n_iter=w.n_iter,
-                 comm_rate_gbs=args.comm_rate_gbs)
+                 comm_rate_gbs=args.comm_rate_gbs, b_layout=args.b_layout)
 
     # untimed warmup steps, then exactly `steps` timed steps
     occ.run_overlap(A, B, C, reps=args.warmup, warmup=0, **knobs, **comm) if args.warmup > 0 else None
@@ -209,18 +213,21 @@ def main():
 
     gemm_tflops = w.gemm_flops / (r["t_gemm_ms"] * 1e-3) / 1e12
     comm_gbs = w.comm_bytes / (r["t_comm_ms"] * 1e-3) / 1e9
-    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, args.variant, args.gemm_grid)
+    variant = args.variant if args.variant or args.b_layout == "nk" else occ.KN_VARIANTS[0]
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, variant, args.gemm_grid)
+    gemm_name = "occ_gemm" if args.b_layout == "nk" else "occ_gemm_kn"
+    traffic_key = w.name if args.b_layout == "nk" else w.name + "_kn"
     gemm_bound_mb = w.M <= 16
     dominant_gemm = r["t_gemm_ms"] >= r["t_comm_ms"]
     if dominant_gemm and not gemm_bound_mb:
         roof = {"bound": "mfma", "achieved": round(gemm_tflops, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
-                "traffic": measured_traffic("gemm", w.name), "kernel": "occ_gemm variant %d" % plan["kernel_id"]}
+                "traffic": measured_traffic("gemm", traffic_key), "kernel": "%s variant %d" % (gemm_name, plan["kernel_id"])}
     elif dominant_gemm:
         gbs = w.gemm_bytes / (r["t_gemm_ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("gemm", w.name),
-                "kernel": "occ_gemm skinny"}
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("gemm", traffic_key),
+                "kernel": "%s variant %d" % (gemm_name, plan["kernel_id"])}
     else:
         roof = {"bound": "hbm", "achieved": round(comm_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(comm_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("comm", w.name),
@@ -240,8 +247,8 @@ def main():
         "dtype": "bf16 (fp32 accumulate) + f32",
         "data": "synthetic",
         "config": {
-            "workload": "%s: bf16 GEMM %dx%dx%d (B as N x K) + %s, %d iterations per schedule"
-                        % (w.name, w.M, w.N, w.K,
+            "workload": "%s: bf16 GEMM %dx%dx%d (B as %s) + %s, %d iterations per schedule"
+                        % (w.name, w.M, w.N, w.K, "N x K" if args.b_layout == "nk" else "K x N",
                            ("share_reduce %d x %d fp32" % (w.nchunks, w.length)) if w.comm == "reduce"
                            else ("share_permute %d x %d B" % (w.nchunks, w.chunk_bytes)), w.n_iter),
             "lds_pad_bytes": args.pad_kib << 10,
@@ -291,7 +298,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the oracle on a bounded sample ...")
-        line["cpu_baseline"] = cpu_baseline(w, A, B, comm, args.cpu_budget)
+        line["cpu_baseline"] = cpu_baseline(w, A, B, comm, args.cpu_budget, args.b_layout)
     print(json.dumps(line), flush=True)
 
 

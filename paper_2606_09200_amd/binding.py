@@ -341,10 +341,10 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
 
 
 def occ_overlap_tune(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
-                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3):
+                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3, b_layout="nk"):
     """Adaptive knob choice (see occ.h).  Returns (chosen knobs, result dict, prefer_sequential)."""
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, 0, gemm_variant, 0, 0, 0,
-                          0, n_iter, reps, warmup, 0, None, None)
+                          0, n_iter, reps, warmup, 0, None, None, 0.0, b_layout)
     res = occ_overlap_result()
     pref = ctypes.c_int(0)
     _check(lib().occ_overlap_tune(ctypes.byref(cfg), int(tune_reps), ctypes.byref(res),

@@ -45,8 +45,10 @@ def setup(w, dev):
 
 
 def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs):
-    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0),
-                                   knobs.get("gemm_grid", 0))
+    variant = knobs.get("gemm_variant", 0)
+    if knobs.get("b_layout", "nk") == "kn" and variant == 0:
+        variant = occ.KN_VARIANTS[0]
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, variant, knobs.get("gemm_grid", 0))
     row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
            "gemm_grid": plan["grid"],
            "gemm_variant": plan["kernel_id"], "gemm_tile_lds": plan["tile_lds_bytes"],
@@ -86,7 +88,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 
 
 def table(rows):
-    cols = ["workload", "graph", "pace_all", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
+    cols = ["workload", "b_layout", "graph", "pace_all", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
             "comm_rate_gbs", "gemm_wg_per_cu", "gemm_wg_per_cu_achieved", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "comm_ovl_us", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
@@ -119,6 +121,9 @@ def main(argv=None):
                     help="comma list of persistent GEMM grid caps to run each workload with "
                          "(0 = one workgroup per tile); the rows then show the engine clock "
                          "against the number of CUs the GEMM keeps busy")
+    ap.add_argument("--b-layout", default="nk", choices=["nk", "kn"],
+                    help="GEMM B stored N x K (occ_gemm) or K x N (occ_gemm_kn: the automatic "
+                         "variant only, so the pad and tile-size points are skipped)")
     ap.add_argument("--pace-all", action="store_true",
                     help="apply --rates to every schedule (OCC_RUN_PACE_ALL): emulates a collective "
                          "whose time is set by inter-GPU links")
@@ -128,11 +133,15 @@ def main(argv=None):
     for name in a.workloads.split(","):
         w = WORKLOADS[name]
         A, B, C, comm = setup(w, dev)
+        if a.b_layout == "kn":
+            B = B.t().contiguous()  # the same op(B), stored K x N
         # The pad sweep runs with the default tile (128 KiB of LDS: only small
         # pads fit) and with tiles small enough for the pad to set residency:
         # 128x256x32 (48 KiB, two per CU), 128x128x64 (96 KiB, three stages) and
         # the paper's opt2 64x64x64.
-        if name == "blocks":
+        if a.b_layout == "kn":
+            points = [dict(gemm_variant=0, gemm_grid=int(g)) for g in (a.gemm_grids or "0").split(",")]
+        elif name == "blocks":
             # the paper's two tiles (opt1 64x64x32, opt2 64x64x64) over the
             # thread-block counts of its tile-size study
             points = [dict(gemm_variant=v, gemm_grid=x * x) for v in (6, 7) for x in BLOCK_COUNTS]
@@ -151,7 +160,9 @@ def main(argv=None):
                 for pad in w.pads:
                     for prio in prios:
                         fl = (occ.OCC_RUN_GRAPH if a.graph else 0) | (occ.OCC_RUN_PACE_ALL if a.pace_all else 0)
-                        row = measure(w, A, B, C, comm, pad, prio, dev, flags=fl, **knobs, **ex)
+                        row = measure(w, A, B, C, comm, pad, prio, dev, flags=fl, b_layout=a.b_layout,
+                                      **knobs, **ex)
+                        row["b_layout"] = a.b_layout
                         row["graph"] = bool(a.graph)
                         row["pace_all"] = bool(a.pace_all)
                         row["comm_rate_gbs"] = ex["comm_rate_gbs"]
@@ -163,7 +174,7 @@ def main(argv=None):
                         print(json.dumps(row), flush=True)
         if a.tune and name not in ("sweep", "blocks"):
             knobs, r, prefer_seq = occ.occ_overlap_tune(A, B, C, n_iter=w.n_iter, reps=5, warmup=2,
-                                                        tune_reps=3, **comm)
+                                                        tune_reps=3, b_layout=a.b_layout, **comm)
             row = {"workload": w.name + " (tuned)", "gemm_variant": "auto", "gemm_grid": knobs["gemm_grid"],
                    "pad_kib": knobs["lds_bytes"] >> 10, "comm_priority": knobs["comm_priority"],
                    "comm_wgs": knobs["comm_wgs"], "t_seq_ms": round(r["t_seq_ms"], 4),

@@ -262,3 +262,17 @@ def test_overlap_with_kn_b_matches_plain_calls():
     with pytest.raises(occ.OccError):                   # a variant that reads N x K
         occ.run_overlap(A, Bkn, C, bufs=chunks, out=out, b_layout="kn", gemm_variant=16,
                         n_iter=1, reps=1, warmup=0)
+
+
+def test_overlap_tune_with_kn_b_keeps_results():
+    A, B, C, chunks, out = tiny_reduce_setup(M=1024, N=1024, K=2048, nchunks=4, length=1 << 22)
+    Bkn = B.t().contiguous()
+    C_ref = torch.empty_like(C)
+    occ.occ_gemm_kn(A, Bkn, C_ref)
+    knobs, r, prefer_seq = occ.occ_overlap_tune(A, Bkn, C, bufs=chunks, out=out, n_iter=4, reps=2,
+                                                warmup=1, tune_reps=1, b_layout="kn")
+    torch.cuda.synchronize()
+    assert r["t_ovl_ms"] > 0 and r["t_seq_ms"] > 0
+    assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
+    assert np.array_equal(out.cpu().numpy().view(np.uint32),
+                          oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
