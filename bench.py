@@ -135,7 +135,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the overlap method is per device and this build "
+        print("bench.py measures one GPU only: the overlap method is per device and the library "
               "has no multi-GPU path; run it with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
