@@ -185,6 +185,19 @@ def main():
     cores = trace.coresidency(recs)
     resid = trace.residency(recs)
 
+    # the same GEMM through torch.mm (hipBLASLt) on the same operands: a
+    # same-run reference for the GEMM, context only
+    ref_mm = (lambda: torch.mm(A, B.t(), out=C)) if args.b_layout == "nk" else (lambda: torch.mm(A, B, out=C))
+    for _ in range(3):
+        ref_mm()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        ref_mm()
+    e1.record()
+    torch.cuda.synchronize()
+    hipblaslt_ms = e0.elapsed_time(e1) / 10
+
     # a plain 1 GiB device-to-device copy: a measured HBM ceiling beside the spec peak
     src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
@@ -273,6 +286,7 @@ def main():
         "t_comm_ms": round(r["t_comm_ms"], 4),
         "ideal_ovl_ms": round(w.n_iter * max(r["t_gemm_ms"], r["t_comm_ms"]) + min(r["t_gemm_ms"], r["t_comm_ms"]), 4),
         "gemm_tflops": round(gemm_tflops, 1),
+        "gemm_hipblaslt_tflops": round(w.gemm_flops / (hipblaslt_ms * 1e-3) / 1e12, 1),
         "gemm_mfma_frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
         "comm_gbs": round(comm_gbs, 1),
         "comm_hbm_frac": round(comm_gbs / PEAK_HBM_GBS, 4),
