@@ -56,6 +56,12 @@ def make_inputs(w, dev):
     from paper_2606_09200_amd import inputs
     A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_a=w.std_a, std_b=w.std_b,
                                 seed_b=w.seed_b, device=dev)
+    if w.comm == "reduce_own":
+        # one GEMM output per iteration; each iteration's collective reduces its own
+        C = torch.empty((w.n_iter, w.M, w.N), device=dev, dtype=torch.bfloat16)
+        comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),
+                    out=torch.empty(w.length, device=dev), reduce_own=True)
+        return A, B, C, comm
     C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
     if w.comm == "reduce":
         comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),
@@ -67,7 +73,7 @@ def make_inputs(w, dev):
     return A, B, C, comm
 
 
-def cpu_baseline(w, A, B, comm, budget_s, b_layout="nk"):
+def cpu_baseline(w, A, B, C, comm, budget_s, b_layout="nk"):
     """The oracle, as it stands, on a bounded sample of the same step, scaled
     to one sequential pass of n_iter iterations (ms)."""
     import numpy as np
@@ -90,7 +96,15 @@ def cpu_baseline(w, A, B, comm, budget_s, b_layout="nk"):
     macs_sample = tiles * min(64, w.M) * min(64, w.N) * w.K
     gemm_full_s = t_gemm_sample * (w.M * w.N * w.K) / macs_sample
     # comm: a contiguous slice of the same payload
-    if w.comm == "reduce":
+    if w.comm == "reduce_own":
+        n = min(w.length, 1 << 22)
+        own = C[0].reshape(-1)[:n].cpu()
+        sl = comm["bufs"][:, :n].cpu().numpy()
+        t1 = time.perf_counter()
+        oracle.chunk_sum_own_f32(own, sl)
+        comm_full_s = (time.perf_counter() - t1) * w.length / n
+        comm_desc = "bf16 own term + %d x %d fp32 chunk sum" % (w.nchunks, n)
+    elif w.comm == "reduce":
         ch = comm["bufs"]
         n = min(w.length, 1 << 22)
         sl = ch[:, :n].cpu().numpy()
@@ -120,7 +134,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="cb", choices=["tiny", "cb", "mb", "a2a"])
+    ap.add_argument("--workload", default="cb", choices=["tiny", "cb", "mb", "a2a", "cb_own"])
     ap.add_argument("--pad-kib", type=int, default=0, help="extra LDS per GEMM workgroup")
     ap.add_argument("--priority", type=int, default=3, help="comm kernel wave priority 0..3")
     ap.add_argument("--variant", type=int, default=0, help="GEMM kernel variant (0 = auto)")
@@ -187,7 +201,8 @@ def main():
 
     # the same GEMM through torch.mm (hipBLASLt) on the same operands: a
     # same-run reference for the GEMM, context only
-    ref_mm = (lambda: torch.mm(A, B.t(), out=C)) if args.b_layout == "nk" else (lambda: torch.mm(A, B, out=C))
+    C2 = C[0] if C.dim() == 3 else C
+    ref_mm = (lambda: torch.mm(A, B.t(), out=C2)) if args.b_layout == "nk" else (lambda: torch.mm(A, B, out=C2))
     for _ in range(3):
         ref_mm()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -263,6 +278,8 @@ def main():
             "workload": "%s: bf16 GEMM %dx%dx%d (B as %s) + %s, %d iterations per schedule"
                         % (w.name, w.M, w.N, w.K, "N x K" if args.b_layout == "nk" else "K x N",
                            ("share_reduce %d x %d fp32" % (w.nchunks, w.length)) if w.comm == "reduce"
+                           else ("share_reduce_own of C_i + %d x %d fp32" % (w.nchunks, w.length))
+                           if w.comm == "reduce_own"
                            else ("share_permute %d x %d B" % (w.nchunks, w.chunk_bytes)), w.n_iter),
             "lds_pad_bytes": args.pad_kib << 10,
             "comm_wave_priority": args.priority,
@@ -312,7 +329,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("cpu baseline: timing the oracle on a bounded sample ...")
-        line["cpu_baseline"] = cpu_baseline(w, A, B, comm, args.cpu_budget, args.b_layout)
+        line["cpu_baseline"] = cpu_baseline(w, A, B, C, comm, args.cpu_budget, args.b_layout)
     print(json.dumps(line), flush=True)
 
 

@@ -219,13 +219,36 @@ int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *ou
 int share_permute(const void *src, void *dst, const int32_t *perm, int nchunks, size_t chunk_bytes,
                   void *stream);
 
+/*
+ * share_reduce_own -- the allreduce share whose first term is this GPU's own
+ * contribution held in bf16 (for instance the GEMM's output C):
+ *   out[j] = (((f32(own[j]) + peers[0][j]) + peers[1][j]) + ...) + peers[n-1][j]
+ * in IEEE binary32, strict left-to-right, f32() the exact widening of a bf16
+ * bit pattern.  Bit-identical to that definition.
+ *   own   : device bf16 buffer of len elements (2-byte aligned).
+ *   peers : HOST array of npeers device fp32 pointers, 0 <= npeers <= 63
+ *           (may be NULL when npeers == 0).
+ *   out   : device fp32 buffer of len elements; must not overlap own or any
+ *           peer.
+ *   wgs, priority : as share_reduce_ex.
+ * len == 0 is a no-op.  own 8-byte aligned with out and peers 16-byte aligned
+ * takes the vectorised path.
+ */
+int share_reduce_own(const void *own, const float *const *peers, int npeers, size_t len, float *out,
+                     int wgs, int priority, void *stream);
+
 /* share_permute_ex -- share_permute with `wgs` and `priority` as share_reduce_ex. */
 int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes, int wgs, int priority, void *stream);
 
 /* ------------------------------------------------------------------ schedule */
 
-enum { OCC_COMM_REDUCE = 0, OCC_COMM_PERMUTE = 1 };
+/* OCC_COMM_REDUCE_OWN: the collective consumes the GEMM's output.  C then
+   holds n_iter consecutive M x N outputs (M*N a multiple of 8): iteration i's
+   GEMM writes C_i = C + i*M*N and iteration i's collective is
+   share_reduce_own(C_i, bufs, nchunks, len = M*N, out); the per-iteration
+   buffers keep GEMM i+1 from overwriting what collective i still reads. */
+enum { OCC_COMM_REDUCE = 0, OCC_COMM_PERMUTE = 1, OCC_COMM_REDUCE_OWN = 2 };
 
 /* run_overlap flags: which passes to time (no pass bit set means all three),
    and OCC_RUN_GRAPH: capture the sequential and the overlapped schedule into
@@ -249,7 +272,9 @@ typedef struct occ_overlap_cfg {
   int gemm_grid;            /* 0: one workgroup per tile; > 0: persistent grid cap */
   int gemm_priority;        /* wave priority of the GEMM kernel, 0 (normal) .. 3 */
   /* (gemm_b_layout is at the end of the structure) */
-  /* K_c: as share_reduce (comm_kind 0) or share_permute (comm_kind 1) */
+  /* K_c: as share_reduce (comm_kind 0), share_permute (comm_kind 1) or
+     share_reduce_own of the GEMM's output (comm_kind 2, bufs/nchunks = the
+     fp32 peer chunks) */
   int comm_kind;
   const float *const *bufs; /* host array of device pointers */
   int nchunks;
@@ -358,7 +383,7 @@ const char *occ_strerror(int status);
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
 #define OCC_VERSION_MAJOR 1
-#define OCC_VERSION_MINOR 2
+#define OCC_VERSION_MINOR 3
 int occ_version(void);
 
 #ifdef __cplusplus

@@ -39,6 +39,10 @@ def _load():
         lib.oracle_chunk_sum_f32.argtypes = [
             ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p]
         lib.oracle_chunk_sum_f32.restype = None
+        lib.oracle_chunk_sum_own_f32.argtypes = [
+            ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_size_t,
+            ctypes.c_void_p]
+        lib.oracle_chunk_sum_own_f32.restype = None
         lib.oracle_permute.argtypes = [
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t]
         lib.oracle_permute.restype = None
@@ -111,6 +115,19 @@ def chunk_sum_f32(chunks):
     out = np.empty(length, dtype=np.float32)
     ptrs = (ctypes.c_void_p * n)(*[c[i].ctypes.data for i in range(n)])
     _load().oracle_chunk_sum_f32(ptrs, n, length, out.ctypes.data)
+    return out
+
+
+def chunk_sum_own_f32(own, chunks):
+    """Fixed-order binary32 sum own + chunks[0] + ... + chunks[n-1], where
+    ``own`` holds bfloat16 bit patterns (uint16, or a bfloat16 tensor) of the
+    chunk length and ``chunks`` is n x len float32 (n may be 0)."""
+    o = np.ascontiguousarray(_u16(own).reshape(-1))
+    c = np.ascontiguousarray(np.asarray(chunks, dtype=np.float32)).reshape(-1, o.size)
+    n, length = c.shape
+    out = np.empty(length, dtype=np.float32)
+    ptrs = (ctypes.c_void_p * max(1, n))(*[c[i].ctypes.data for i in range(n)])
+    _load().oracle_chunk_sum_own_f32(o.ctypes.data, ptrs, n, length, out.ctypes.data)
     return out
 
 

@@ -17,7 +17,8 @@
  *     aggregated across GPUs): element-wise sum of the chunks in binary32,
  *     strict left-to-right order c0 + c1 + ... + c_{n-1}.  The fixed order
  *     and binary32 arithmetic are a requirement of the workload, not of the
- *     paper, which is silent on both.
+ *     paper, which is silent on both.  When this GPU's own term is its bf16
+ *     GEMM output, that term comes first, converted exactly to binary32.
  *   - Local share of an alltoall (Background, item 2: tokens are routed
  *     between devices): chunk i of the destination is chunk perm[i] of the
  *     source, byte for byte.
@@ -107,6 +108,25 @@ void oracle_chunk_sum_f32(const float *const *chunks, int nchunks, size_t len, f
   for (long long j = 0; j < (long long)len; ++j) {
     float acc = chunks[0][j];
     for (int c = 1; c < nchunks; ++c) acc = acc + chunks[c][j];
+    out[j] = acc;
+  }
+}
+
+/*
+ * The same share when this GPU's own contribution is bf16 (its GEMM output):
+ * out[j] = (((own[j] + c_0[j]) + c_1[j]) + ...) + c_{n-1}[j], binary32, with
+ * own[j] first made a binary32 by the definition of bfloat16: its 16 bits are
+ * the high half of the binary32 word (exact for every value, NaN payloads
+ * included).  n may be 0 (out = own as binary32).
+ */
+void oracle_chunk_sum_own_f32(const uint16_t *own, const float *const *chunks, int nchunks, size_t len,
+                              float *out) {
+#pragma omp parallel for schedule(static)
+  for (long long j = 0; j < (long long)len; ++j) {
+    uint32_t w = (uint32_t)own[j] << 16;
+    float acc;
+    memcpy(&acc, &w, sizeof acc);
+    for (int c = 0; c < nchunks; ++c) acc = acc + chunks[c][j];
     out[j] = acc;
   }
 }

@@ -18,7 +18,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libocc.so")
 
 OCC_OK, OCC_EINVAL, OCC_ELDS, OCC_EPERM, OCC_EALIAS, OCC_EHIP, OCC_ENODEV = 0, -1, -2, -3, -4, -5, -6
-OCC_COMM_REDUCE, OCC_COMM_PERMUTE = 0, 1
+OCC_COMM_REDUCE, OCC_COMM_PERMUTE, OCC_COMM_REDUCE_OWN = 0, 1, 2
 OCC_RUN_SEQ, OCC_RUN_OVL, OCC_RUN_ISO, OCC_RUN_GRAPH, OCC_RUN_PACE_ALL = 1, 2, 4, 8, 16
 GEMM_VARIANTS = {
     0: "auto", 1: "256x256x64 4w", 2: "256x256x64 8w", 3: "256x128x64 4w",
@@ -36,7 +36,7 @@ GEMM_VARIANTS = {
 }
 KN_VARIANTS = (32,)       # take B stored K x N (occ_gemm_kn_ex only)
 SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
-ABI_VERSION = (1, 2)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+ABI_VERSION = (1, 3)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -93,6 +93,8 @@ _SIGS = {
     "share_reduce": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, _P],
     "share_reduce_ex": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, ctypes.c_int,
                         ctypes.c_int, _P],
+    "share_reduce_own": [_P, ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, ctypes.c_int,
+                         ctypes.c_int, _P],
     "share_permute": [_P, _P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t, _P],
     "share_permute_ex": [_P, _P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int, ctypes.c_size_t,
                          ctypes.c_int, ctypes.c_int, _P],
@@ -234,6 +236,32 @@ def share_reduce(bufs, out, stream=None, wgs=0, priority=0):
     return out
 
 
+def _peer_ptrs(peers, length):
+    """Host array of fp32 peer-chunk pointers (possibly none) of `length` elements each."""
+    if peers is None:
+        peers = []
+    elif isinstance(peers, torch.Tensor):
+        peers = list(peers.unbind(0)) if peers.dim() == 2 else [peers]
+    for b in peers:
+        if b.dtype != torch.float32 or not b.is_cuda or not b.is_contiguous() or b.numel() != length:
+            raise ValueError("peer chunks must be contiguous float32 GPU tensors of the own length")
+    arr = (ctypes.c_void_p * max(1, len(peers)))(*[b.data_ptr() for b in peers])
+    return arr, len(peers)
+
+
+def share_reduce_own(own, peers, out, stream=None, wgs=0, priority=0):
+    """out = f32(own) + peers[0] + peers[1] + ... (binary32, left to right); own is bf16."""
+    if own.dtype != torch.bfloat16 or not own.is_cuda or not own.is_contiguous():
+        raise ValueError("own must be a contiguous bfloat16 GPU tensor")
+    length = own.numel()
+    arr, n = _peer_ptrs(peers, length)
+    if out.dtype != torch.float32 or not out.is_cuda or out.numel() != length:
+        raise ValueError("out must be a float32 GPU tensor of the own length")
+    _check(lib().share_reduce_own(_ptr(own), arr, n, length, _ptr(out), int(wgs), int(priority),
+                                  _stream(stream)), "share_reduce_own")
+    return out
+
+
 def _perm_arr(perm):
     p = [int(x) for x in (perm.tolist() if hasattr(perm, "tolist") else perm)]
     return (ctypes.c_int32 * max(1, len(p)))(*p), len(p)
@@ -274,10 +302,16 @@ def decode_wg_trace(wg_trace):
 
 def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant, gemm_grid,
               gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace,
-              comm_rate_gbs=0.0, b_layout="nk"):
+              comm_rate_gbs=0.0, b_layout="nk", reduce_own=False):
     if b_layout not in ("nk", "kn"):
         raise ValueError("b_layout must be 'nk' or 'kn'")
-    M, N, K = _gemm_args(A, B, C, b_kn=b_layout == "kn")
+    if reduce_own:
+        # C holds one M x N output per iteration; the collective reduces its own
+        if C.dim() != 3 or C.shape[0] != n_iter:
+            raise ValueError("with reduce_own, C must be (n_iter, M, N)")
+        M, N, K = _gemm_args(A, B, C[0], b_kn=b_layout == "kn")
+    else:
+        M, N, K = _gemm_args(A, B, C, b_kn=b_layout == "kn")
     cfg = occ_overlap_cfg()
     cfg.M, cfg.N, cfg.K = M, N, K
     cfg.A, cfg.B, cfg.C = _ptr(A).value, _ptr(B).value, _ptr(C).value
@@ -286,7 +320,15 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
     cfg.comm_rate_gbs = float(comm_rate_gbs)
     cfg.gemm_b_layout = 1 if b_layout == "kn" else 0
     keep = []
-    if bufs is not None:
+    if reduce_own:
+        arr, n = _peer_ptrs(bufs, M * N)
+        keep.append(arr)
+        cfg.comm_kind = OCC_COMM_REDUCE_OWN
+        cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+        cfg.nchunks, cfg.len, cfg.out = n, M * N, _ptr(out).value
+        if out.numel() != M * N or out.dtype != torch.float32:
+            raise ValueError("out must be float32 of M*N elements")
+    elif bufs is not None:
         arr, n, length = _chunk_ptrs(bufs)
         keep.append(arr)
         cfg.comm_kind = OCC_COMM_REDUCE
@@ -321,7 +363,7 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
 def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
                 lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0,
                 comm_priority=3, n_iter=10, reps=20, warmup=10, flags=0, timeline=None,
-                wg_trace=None, comm_rate_gbs=0.0, b_layout="nk"):
+                wg_trace=None, comm_rate_gbs=0.0, b_layout="nk", reduce_own=False):
     """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
 
     Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
@@ -330,21 +372,26 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
     optional int32 GPU tensor of 4 + 12*cap entries (see occ_overlap_cfg.wg_trace).
     ``comm_rate_gbs``: bandwidth pacing of the collective in the overlapped
     schedule (0 = full speed).  ``b_layout``: "nk" (B is N x K, C = A B^T) or
-    "kn" (B is K x N, C = A B).  Returns the occ_overlap_result fields as a dict.
+    "kn" (B is K x N, C = A B).  ``reduce_own``: the collective consumes the
+    GEMM's output (OCC_COMM_REDUCE_OWN): C is (n_iter, M, N), iteration i's
+    GEMM writes C[i] and its collective is share_reduce_own(C[i], bufs, out)
+    with ``bufs`` the fp32 peer chunks (possibly none).  Returns the
+    occ_overlap_result fields as a dict.
     """
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
                           gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup,
-                          flags, timeline, wg_trace, comm_rate_gbs, b_layout)
+                          flags, timeline, wg_trace, comm_rate_gbs, b_layout, reduce_own)
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}
 
 
 def occ_overlap_tune(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
-                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3, b_layout="nk"):
+                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3, b_layout="nk",
+                     reduce_own=False):
     """Adaptive knob choice (see occ.h).  Returns (chosen knobs, result dict, prefer_sequential)."""
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, 0, gemm_variant, 0, 0, 0,
-                          0, n_iter, reps, warmup, 0, None, None, 0.0, b_layout)
+                          0, n_iter, reps, warmup, 0, None, None, 0.0, b_layout, reduce_own)
     res = occ_overlap_result()
     pref = ctypes.c_int(0)
     _check(lib().occ_overlap_tune(ctypes.byref(cfg), int(tune_reps), ctypes.byref(res),

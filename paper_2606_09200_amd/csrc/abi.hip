@@ -44,6 +44,19 @@ int validate_reduce(const float *const *bufs, int nchunks, size_t len, const flo
   return OCC_OK;
 }
 
+int validate_reduce_own(const void *own, const float *const *peers, int npeers, size_t len,
+                        const float *out) {
+  if (npeers < 0 || npeers > kMaxReduceChunks - 1 || (npeers > 0 && peers == nullptr)) return OCC_EINVAL;
+  if (len == 0) return OCC_OK;
+  if (own == nullptr || !aligned(own, 2) || out == nullptr || !aligned(out, 4)) return OCC_EINVAL;
+  for (int i = 0; i < npeers; ++i)
+    if (peers[i] == nullptr || !aligned(peers[i], 4)) return OCC_EINVAL;
+  if (overlaps(out, len * 4, own, len * 2)) return OCC_EALIAS;
+  for (int i = 0; i < npeers; ++i)
+    if (overlaps(out, len * 4, peers[i], len * 4)) return OCC_EALIAS;
+  return OCC_OK;
+}
+
 int validate_permute(const void *src, const void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes) {
   if (perm == nullptr || nchunks < 1 || nchunks > kMaxPermuteChunks) return OCC_EINVAL;
@@ -157,6 +170,18 @@ int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *ou
 
 int share_reduce(const float *const *bufs, int nchunks, size_t len, float *out, void *stream) {
   return share_reduce_ex(bufs, nchunks, len, out, 0, 0, stream);
+}
+
+int share_reduce_own(const void *own, const float *const *peers, int npeers, size_t len, float *out,
+                     int wgs, int priority, void *stream) {
+  int st = occ::validate_reduce_own(own, peers, npeers, len, out);
+  if (st != OCC_OK) return st;
+  if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
+  const occ::DeviceInfo *di = nullptr;
+  if (len > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
+  occ::ReduceCall c{peers, npeers, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0,
+                    static_cast<const uint16_t *>(own)};
+  return occ::reduce_launch(c, static_cast<hipStream_t>(stream));
 }
 
 int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunks,

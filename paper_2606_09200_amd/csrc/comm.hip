@@ -21,6 +21,10 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// bf16 bit pattern -> binary32 (exact: the bf16 bits are the high half)
+__device__ __forceinline__ float widen_bf16(uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); }
 
 constexpr int kThreads = 256;
 
@@ -36,9 +40,14 @@ struct ChunkPtrs {
 // without adding bandwidth.  The default grid is one workgroup per CU (one
 // wave per SIMD): as fast as two per CU alone, and a co-running GEMM loses
 // less issue time to one comm wave per SIMD than to two.
-template <int NC, int UNROLL, bool OFF32>
+//
+// OWN: the first term is a bf16 buffer (this GPU's own contribution, e.g. its
+// GEMM output), widened exactly to binary32; the NC (or nchunks) fp32 chunks
+// follow it in order.  Its 8 bytes per position are one load.
+template <int NC, int UNROLL, bool OFF32, bool OWN>
 __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
-                                                              float *__restrict__ out, int prio,
+                                                              float *__restrict__ out,
+                                                              const uint16_t *__restrict__ own, int prio,
                                                               uint32_t pace, KTrace tr) {
   // OFF32: every byte offset the loop forms fits in 32 bits (checked by the
   // host), so each access is a scalar base plus one shared 32-bit lane
@@ -59,20 +68,35 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
   auto st = [&](f32x4 v, I k) {
     __builtin_nontemporal_store(v, reinterpret_cast<f32x4 *>(reinterpret_cast<char *>(out) + k * (I)sizeof(f32x4)));
   };
+  auto ld_own = [&](I k) {
+    const u32x2 w = __builtin_nontemporal_load(
+        reinterpret_cast<const u32x2 *>(reinterpret_cast<const char *>(own) + k * (I)sizeof(u32x2)));
+    f32x4 r;
+    r[0] = widen_bf16(w[0] & 0xFFFFu);
+    r[1] = widen_bf16(w[0] >> 16);
+    r[2] = widen_bf16(w[1] & 0xFFFFu);
+    r[3] = widen_bf16(w[1] >> 16);
+    return r;
+  };
+  constexpr int C0 = OWN ? 0 : 1;  // first fp32 chunk added to the first term
 
   if constexpr (NC > 0) {
     for (bool first = true; i + (UNROLL - 1) * stride < n; i += UNROLL * stride, first = false) {
       if (!first) pace_wait(pc);
-      f32x4 v[NC][UNROLL];
+      f32x4 v[NC][UNROLL], o[UNROLL];
+      if constexpr (OWN) {
+#pragma unroll
+        for (int u = 0; u < UNROLL; ++u) o[u] = ld_own(i + u * stride);
+      }
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
         for (int u = 0; u < UNROLL; ++u) v[c][u] = ld(c, i + u * stride);
 #pragma unroll
       for (int u = 0; u < UNROLL; ++u) {
-        f32x4 acc = v[0][u];
+        f32x4 acc = OWN ? o[u] : v[0][u];
 #pragma unroll
-        for (int c = 1; c < NC; ++c) {
+        for (int c = C0; c < NC; ++c) {
           acc[0] = acc[0] + v[c][u][0];
           acc[1] = acc[1] + v[c][u][1];
           acc[2] = acc[2] + v[c][u][2];
@@ -86,8 +110,8 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
   // known at run time): chunks in batches of 8 loads, folded in order.
   for (bool first = true; i < n; i += stride, first = false) {
     if (NC == 0 && !first) pace_wait(pc);
-    f32x4 acc = ld(0, i);
-    for (int c0 = 1; c0 < nc; c0 += 8) {
+    f32x4 acc = OWN ? ld_own(i) : ld(0, i);
+    for (int c0 = C0; c0 < nc; c0 += 8) {
       f32x4 v[8];
 #pragma unroll
       for (int c = 0; c < 8; ++c)
@@ -110,14 +134,15 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
 // path, or everything when a buffer is not 16-byte aligned).
 __global__ __launch_bounds__(kThreads) void reduce_scalar_kernel(ChunkPtrs cp, int nchunks,
                                                                  size_t first, size_t len,
-                                                                 float *__restrict__ out, int prio,
-                                                                 KTrace tr) {
+                                                                 float *__restrict__ out,
+                                                                 const uint16_t *__restrict__ own,
+                                                                 int prio, KTrace tr) {
   set_wave_priority(prio);
   const TraceStart t0 = trace_begin(tr);
   const size_t stride = (size_t)gridDim.x * kThreads;
   for (size_t j = first + (size_t)blockIdx.x * kThreads + threadIdx.x; j < len; j += stride) {
-    float acc = cp.p[0][j];
-    for (int c = 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
+    float acc = own != nullptr ? widen_bf16(own[j]) : cp.p[0][j];
+    for (int c = own != nullptr ? 0 : 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
     out[j] = acc;
   }
   trace_end(tr, t0);
@@ -213,15 +238,16 @@ uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
 
 }  // namespace
 
-template <bool OFF32>
-void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_t nvec, float *out, int prio,
-                   uint32_t pace, const KTrace &tr) {
-  switch (nchunks) {
-    case 2: hipLaunchKernelGGL((reduce_vec_kernel<2, 4, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
-    case 4: hipLaunchKernelGGL((reduce_vec_kernel<4, 2, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
-    case 8: hipLaunchKernelGGL((reduce_vec_kernel<8, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
-    case 16: hipLaunchKernelGGL((reduce_vec_kernel<16, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
-    default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, prio, pace, tr); break;
+template <bool OFF32, bool OWN>
+void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_t nvec, float *out,
+                   const uint16_t *own, int prio, uint32_t pace, const KTrace &tr) {
+  // instantiations by the number of terms (own + fp32 chunks)
+  switch (nchunks + (OWN ? 1 : 0)) {
+    case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, 4, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 4: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 3 : 4, 2, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 8: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 7 : 8, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 16: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 15 : 16, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
   }
 }
 
@@ -235,7 +261,8 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
   if (c.len == 0) return OCC_OK;
   ChunkPtrs cp;
   memset(&cp, 0, sizeof cp);
-  bool vec = aligned16(c.out);
+  const bool own = c.own != nullptr;
+  bool vec = aligned16(c.out) && (!own || (reinterpret_cast<uintptr_t>(c.own) & 7u) == 0);
   for (int i = 0; i < c.nchunks; ++i) {
     cp.p[i] = c.bufs[i];
     vec = vec && aligned16(c.bufs[i]);
@@ -246,22 +273,30 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
     size_t nvec = c.len / 4;
     if (nvec > 0) {
       int g = clamp_wgs(nvec, wgs);
-      // positions per lane per trip of each instantiation
-      const int unroll = c.nchunks == 2 ? 4 : c.nchunks == 4 ? 2 : 1;
-      const uint32_t pace = pace_ticks((double)g * kThreads * unroll * 16.0 * (c.nchunks + 1), c.rate_gbs);
+      // positions per lane per trip of each instantiation, and the bytes
+      // one position moves
+      const int terms = c.nchunks + (own ? 1 : 0);
+      const int unroll = terms == 2 ? 4 : terms == 4 ? 2 : 1;
+      const double pos_bytes = 16.0 * (c.nchunks + 1) + (own ? 8.0 : 0.0);
+      const uint32_t pace = pace_ticks((double)g * kThreads * unroll * pos_bytes, c.rate_gbs);
       // 32-bit offsets when the largest byte offset the loop can form, (nvec
       // plus one unrolled grid stride) * 16, stays below 2^32
       const bool off32 = ((double)nvec + 4.0 * g * kThreads) * 16.0 < 4294967296.0;
-      if (off32) launch_reduce<true>(c.nchunks, g, s, cp, nvec, c.out, prio, pace, c.trace);
-      else launch_reduce<false>(c.nchunks, g, s, cp, nvec, c.out, prio, pace, c.trace);
+      if (own) {
+        if (off32) launch_reduce<true, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
+        else launch_reduce<false, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
+      } else {
+        if (off32) launch_reduce<true, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, c.trace);
+        else launch_reduce<false, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, c.trace);
+      }
     }
     size_t first = nvec * 4;
     if (first < c.len)
       hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kThreads), 0, s, cp, c.nchunks, first,
-                         c.len, c.out, prio, c.trace);
+                         c.len, c.out, c.own, prio, c.trace);
   } else {
     hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs)), dim3(kThreads), 0, s, cp,
-                       c.nchunks, (size_t)0, c.len, c.out, prio, c.trace);
+                       c.nchunks, (size_t)0, c.len, c.out, c.own, prio, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }

@@ -52,6 +52,9 @@ struct ReduceCall {
   int priority;              // 0..3
   KTrace trace;
   double rate_gbs;           // target bandwidth of the vector path, GB/s; 0 = unpaced
+  // when set: the first term of every sum is this bf16 buffer, widened to
+  // binary32, and bufs holds the nchunks (>= 0) fp32 terms after it
+  const uint16_t *own = nullptr;
 };
 int reduce_launch(const ReduceCall &c, hipStream_t s);
 int reduce_default_wgs(const ReduceCall &c);
@@ -73,6 +76,7 @@ int permute_default_wgs(const PermuteCall &c);
 // ---- validation (host only, no HIP calls) --------------------------------
 int validate_gemm(const void *A, const void *B, const void *C, int M, int N, int K, bool b_kn = false);
 int validate_reduce(const float *const *bufs, int nchunks, size_t len, const float *out);
+int validate_reduce_own(const void *own, const float *const *peers, int npeers, size_t len, const float *out);
 int validate_permute(const void *src, const void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes);
 

@@ -72,8 +72,13 @@ struct Launcher {
   PermuteCall p;
   int kind;
 
-  int gemm(hipStream_t s, KTrace t) {
+  // own: iteration i's GEMM writes its own output C_i (C + i*M*N), which
+  // iteration i's collective reduces as its first term
+  bool own = false;
+  void *c_iter(int i) const { return static_cast<uint16_t *>(g.C) + (own ? (size_t)i * g.M * g.N : 0); }
+  int gemm(hipStream_t s, KTrace t, int i) {
     GemmCall c = g;
+    c.C = c_iter(i);
     c.trace = t;
     return gemm_launch(c, s);
   }
@@ -81,10 +86,11 @@ struct Launcher {
   // sequential schedule and the isolated timings do too when pace_all.
   double rate_gbs;
   bool pace_all;
-  int comm(hipStream_t s, KTrace t, bool paced) {
+  int comm(hipStream_t s, KTrace t, bool paced, int i) {
     paced = paced || pace_all;
-    if (kind == OCC_COMM_REDUCE) {
+    if (kind == OCC_COMM_REDUCE || kind == OCC_COMM_REDUCE_OWN) {
       ReduceCall c = r;
+      if (own) c.own = static_cast<const uint16_t *>(c_iter(i));
       c.trace = t;
       c.rate_gbs = paced ? rate_gbs : 0.0;
       return reduce_launch(c, s);
@@ -118,7 +124,19 @@ int validate_cfg(const occ_overlap_cfg *c) {
     return a0 < b0 + bn && b0 < a0 + an;
   };
   size_t abytes = (size_t)c->M * c->K * 2, bbytes = (size_t)c->N * c->K * 2;
-  if (c->comm_kind == OCC_COMM_REDUCE) {
+  if (c->comm_kind == OCC_COMM_REDUCE_OWN) {
+    // C holds n_iter outputs of M*N each, every one 16-byte aligned; the
+    // collective reduces C_i (len = M*N) and the fp32 peer chunks
+    const size_t mn = (size_t)c->M * c->N;
+    if (mn == 0 || mn % 8 != 0 || c->len != mn) return OCC_EINVAL;
+    OCC_TRY(validate_reduce_own(c->C, c->bufs, c->nchunks, c->len, c->out));
+    const size_t call = cbytes * (size_t)c->n_iter, lb = c->len * 4;
+    for (int i = 0; i < c->nchunks; ++i)
+      if (hit(c->C, call, c->bufs[i], lb)) return OCC_EALIAS;
+    if (hit(c->C, call, c->out, lb) || hit(c->out, lb, c->A, abytes) || hit(c->out, lb, c->B, bbytes) ||
+        hit(c->C, call, c->A, abytes) || hit(c->C, call, c->B, bbytes))
+      return OCC_EALIAS;
+  } else if (c->comm_kind == OCC_COMM_REDUCE) {
     OCC_TRY(validate_reduce(c->bufs, c->nchunks, c->len, c->out));
     size_t lb = c->len * 4;
     for (int i = 0; i < c->nchunks; ++i)
@@ -146,8 +164,8 @@ namespace {
 // and joins it back, so the compute stream's next operation follows both.
 int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KTrace &off) {
   for (int i = 0; i < n; ++i) {
-    OCC_TRY(L.gemm(s0, off));
-    OCC_TRY(L.comm(s0, off, false));
+    OCC_TRY(L.gemm(s0, off, i));
+    OCC_TRY(L.comm(s0, off, false, i));
   }
   return OCC_OK;
 }
@@ -157,10 +175,10 @@ int enqueue_ovl(Launcher &L, hipStream_t s0, hipStream_t s1, hipEvent_t fork, hi
   OCC_HIP(hipEventRecord(fork, s0));
   OCC_HIP(hipStreamWaitEvent(s1, fork, 0));
   for (int i = 0; i < n; ++i) {
-    OCC_TRY(L.gemm(s0, tg[i]));
+    OCC_TRY(L.gemm(s0, tg[i], i));
     OCC_HIP(hipEventRecord(deps[i], s0));
     OCC_HIP(hipStreamWaitEvent(s1, deps[i], 0));
-    OCC_TRY(L.comm(s1, tc[i], true));
+    OCC_TRY(L.comm(s1, tc[i], true, i));
   }
   // C_{n-1} waits on G_{n-1}, the last GEMM, so the comm stream's end is the
   // end of the schedule; the compute stream waits for it.
@@ -214,6 +232,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
                  c.gemm_priority, off, c.gemm_b_layout == 1};
   L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
+  L.own = c.comm_kind == OCC_COMM_REDUCE_OWN;
+  if (L.own) L.r.own = static_cast<const uint16_t *>(c.C);
   L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
   L.rate_gbs = c.comm_rate_gbs;
   L.pace_all = (c.flags & OCC_RUN_PACE_ALL) != 0;
@@ -224,7 +244,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   res->gemm_grid = plan.grid;
   res->gemm_tile_lds = plan.tile_lds_bytes;
   res->comm_wgs = c.comm_wgs > 0 ? c.comm_wgs
-                  : (c.comm_kind == OCC_COMM_REDUCE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
+                  : (c.comm_kind != OCC_COMM_PERMUTE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
 
   StreamPair *sp = nullptr;
   OCC_TRY(stream_pair(&sp));
@@ -297,9 +317,9 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     if (flags & OCC_RUN_ISO) {
       OCC_HIP(hipEventRecord(iso[0], s0));
       for (int i = 0; i < n && st == OCC_OK; ++i) {
-        st = L.gemm(s0, off);
+        st = L.gemm(s0, off, i);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 1], s0) != hipSuccess) st = OCC_EHIP;
-        if (st == OCC_OK) st = L.comm(s0, off, false);
+        if (st == OCC_OK) st = L.comm(s0, off, false, i);
         if (st == OCC_OK && hipEventRecord(iso[2 * i + 2], s0) != hipSuccess) st = OCC_EHIP;
       }
       OCC_HIP(hipEventSynchronize(iso[2 * n]));

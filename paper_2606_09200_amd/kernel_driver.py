@@ -48,6 +48,11 @@ def main(argv=None):
             run = lambda: torch.mm(A, B, out=C)
         else:
             run = lambda: torch.mm(A, B.t(), out=C)
+    elif w.comm == "reduce_own":
+        own = torch.randn(w.length, device=dev).to(torch.bfloat16)
+        ch = inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev)
+        out = torch.empty(w.length, device=dev)
+        run = lambda: occ.share_reduce_own(own, ch, out)
     elif w.comm == "reduce":
         ch = inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev)
         out = torch.empty(w.length, device=dev)

@@ -33,6 +33,11 @@ PEAK_GBS = 8000.0
 def setup(w, dev):
     A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_a=w.std_a, std_b=w.std_b,
                                 seed_b=w.seed_b, device=dev)
+    if w.comm == "reduce_own":
+        C = torch.empty((w.n_iter, w.M, w.N), device=dev, dtype=torch.bfloat16)
+        comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),
+                    out=torch.empty(w.length, device=dev), reduce_own=True)
+        return A, B, C, comm
     C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
     if w.comm == "reduce":
         comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),

@@ -12,6 +12,10 @@ collectives on 4-8 GPUs) become one GPU's local share of each collective:
                  with an 8 x 2^24 float32 chunk sum: both kernels are HBM-bound;
 * ``a2a``     -- expert-like GEMM 16384 x 14336 x 4096 with a 64 x 4 MiB
                  chunk permutation (the local block of an alltoall);
+* ``cb_own``  -- ``cb`` whose allreduce share consumes the GEMM's output:
+                 iteration i's GEMM writes its own C_i and iteration i's
+                 collective sums C_i (bf16, widened) and 7 fp32 peer chunks of
+                 8192 x 8192 elements;
 * ``sweep``   -- ``cb`` over extra LDS pads {0,16,32,64,96,128} KiB x comm wave
                  priority {normal, high};
 * ``blocks``  -- ``cb`` with the paper's opt1 and opt2 tiles and a persistent
@@ -34,7 +38,7 @@ class Workload:
     M: int
     N: int
     K: int
-    comm: str                 # "reduce" or "permute"
+    comm: str                 # "reduce", "reduce_own" (first term: the GEMM's output) or "permute"
     nchunks: int
     length: int = 0           # float32 elements per chunk (reduce)
     chunk_bytes: int = 0      # bytes per chunk (permute)
@@ -58,6 +62,8 @@ class Workload:
     def comm_bytes(self):
         if self.comm == "reduce":
             return 4.0 * self.length * (self.nchunks + 1)
+        if self.comm == "reduce_own":   # bf16 own term + nchunks fp32 peers + fp32 out
+            return 2.0 * self.length + 4.0 * self.length * (self.nchunks + 1)
         return 2.0 * self.nchunks * self.chunk_bytes
 
 
@@ -70,6 +76,8 @@ WORKLOADS = {
                    std_b=0.02, seed_b=4, priorities=(0, 3)),
     "a2a": Workload("a2a", 16384, 14336, 4096, "permute", 64, chunk_bytes=4 * MIB,
                     priorities=(0, 3)),
+    "cb_own": Workload("cb_own", 8192, 8192, 8192, "reduce_own", 7, length=8192 * 8192,
+                       priorities=(0, 3)),
     "sweep": Workload("sweep", 8192, 8192, 8192, "reduce", 8, length=1 << 25,
                       pads=tuple(p * KIB for p in (0, 16, 32, 64, 96, 128)),
                       priorities=(0, 3)),

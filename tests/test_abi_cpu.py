@@ -39,9 +39,9 @@ def test_strerror_and_version(L):
     for code in range(0, -7, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == binding.ABI_VERSION == (1, 2)
+    assert binding.occ_version() == binding.ABI_VERSION == (1, 3)
     hdr = open(HEADER).read()
-    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 2" in hdr
+    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 3" in hdr
 
 
 P = ctypes.c_void_p
@@ -84,6 +84,23 @@ def test_reduce_argument_errors(L):
     assert L.share_reduce(odd, 2, 16, out, None) == -1                # not 4-byte aligned
     assert L.share_reduce_ex(arr, 2, 16, out, 0, 4, None) == -1       # priority out of range
     assert L.share_reduce_ex(arr, 2, 16, out, -1, 0, None) == -1
+
+
+def test_reduce_own_argument_errors(L):
+    arr = (ctypes.c_void_p * 64)(*([0x100000 * (i + 1) for i in range(64)]))
+    own, out = P(0x9000000), P(0xA000000)
+    assert L.share_reduce_own(own, arr, -1, 16, out, 0, 0, None) == -1
+    assert L.share_reduce_own(own, arr, 64, 16, out, 0, 0, None) == -1        # 1 + 64 terms
+    assert L.share_reduce_own(own, None, 2, 16, out, 0, 0, None) == -1
+    assert L.share_reduce_own(None, arr, 2, 16, out, 0, 0, None) == -1
+    assert L.share_reduce_own(P(0x9000001), arr, 2, 16, out, 0, 0, None) == -1  # own not 2-byte aligned
+    assert L.share_reduce_own(own, arr, 2, 16, P(0x9000000 + 8), 0, 0, None) == -4  # out over own
+    assert L.share_reduce_own(own, arr, 2, 16, P(0x100000 + 4), 0, 0, None) == -4   # out over a peer
+    assert L.share_reduce_own(own, arr, 2, 16, out, 0, 4, None) == -1         # priority
+    assert L.share_reduce_own(own, arr, 2, 16, out, -1, 0, None) == -1
+    assert L.share_reduce_own(own, None, 0, 0, out, 0, 0, None) == 0          # len 0: no-op
+    # valid arguments pass validation (and then need a device)
+    assert L.share_reduce_own(own, None, 0, 16, out, 0, 0, None) not in (-1, -4)
 
 
 def test_permute_argument_errors(L):
@@ -133,6 +150,17 @@ def test_run_overlap_argument_errors(L):
     cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
     cfg.gemm_b_layout = 2                                                 # neither N x K nor K x N
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.gemm_b_layout = 0
+    cfg.comm_kind, cfg.len = 2, 32                                        # own reduce: len must be M*N
+    cfg.out = 0x40000
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.len = 64
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) != -1      # 8x8 outputs, len 64
+    cfg.out = 0x3000 + 2 * 64 * 2 - 8                                     # out inside C_1 (n_iter = 2)
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -4
+    cfg.M, cfg.N, cfg.len, cfg.out = 3, 3, 9, 0x40000                     # M*N not a multiple of 8
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.M, cfg.N, cfg.len, cfg.comm_kind, cfg.out = 8, 8, 64, 0, 0x30000
     cfg.gemm_b_layout, cfg.N = 1, 12                                      # K x N needs N % 8 == 0
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
     cfg.N = 8

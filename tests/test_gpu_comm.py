@@ -34,6 +34,81 @@ def u32(x):
     return np.asarray(x, dtype=np.float32).view(np.uint32)
 
 
+def own_bits(length, seed):
+    """bf16 bit patterns of N(0,1) samples (no signalling NaNs)."""
+    g = torch.Generator().manual_seed(seed)
+    return torch.randn(length, generator=g).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def gpu_reduce_own(own_host, peers_host, own_offset=0, offset=0, wgs=0, priority=0):
+    """share_reduce_own on device copies; `own_offset` bf16 elements and
+    `offset` floats into their buffers (to exercise misalignment)."""
+    n, length = peers_host.shape
+    ostore = torch.zeros(length + own_offset + 8, dtype=torch.int16, device=DEV)
+    ostore[own_offset:own_offset + length] = torch.from_numpy(own_host.view(np.int16)).to(DEV)
+    own = ostore[own_offset:own_offset + length].view(torch.bfloat16)
+    store = torch.zeros((max(n, 1), length + offset + 4), dtype=torch.float32, device=DEV)
+    if n:
+        store[:n, offset:offset + length] = torch.from_numpy(np.ascontiguousarray(peers_host)).to(DEV)
+    peers = [store[i, offset:offset + length] for i in range(n)]
+    out_store = torch.full((length + offset + 4,), float("nan"), dtype=torch.float32, device=DEV)
+    out = out_store[offset:offset + length]
+    occ.share_reduce_own(own, peers, out, wgs=wgs, priority=priority)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.parametrize("n", [0, 1, 3, 5, 7, 15, 20, 63])
+@pytest.mark.parametrize("length", [1, 3, 4, 1000, 65539])
+def test_reduce_own_bit_exact(n, length):
+    own = own_bits(length, seed=n + 7 * length)
+    peers = inputs.reduce_chunks(n, length, seed=n * 1000 + length).numpy() if n else np.zeros((0, length), np.float32)
+    got = gpu_reduce_own(own, peers)
+    assert np.array_equal(u32(got), u32(oracle.chunk_sum_own_f32(own, peers)))
+
+
+@pytest.mark.parametrize("own_offset,offset", [(1, 0), (2, 0), (3, 1), (0, 2), (4, 0)])
+def test_reduce_own_misaligned_bit_exact(own_offset, offset):
+    own = own_bits(4099, seed=own_offset)
+    peers = inputs.reduce_chunks(7, 4099, seed=11).numpy()
+    got = gpu_reduce_own(own, peers, own_offset=own_offset, offset=offset)
+    assert np.array_equal(u32(got), u32(oracle.chunk_sum_own_f32(own, peers)))
+
+
+def test_reduce_own_order_and_specials():
+    # ((1 + 2^24) - 2^24) = 0: own first, strict left fold; special bf16 values widen exactly
+    own = np.array([0x3F80, 0x7F80, 0xFF80, 0x0001, 0x8000, 0x3F80, 0x4000, 0xC000], dtype=np.uint16)
+    peers = np.zeros((2, 8), dtype=np.float32)
+    peers[:, 0] = [2.0 ** 24, -(2.0 ** 24)]
+    got = gpu_reduce_own(own, peers)
+    ref = oracle.chunk_sum_own_f32(own, peers)
+    assert got[0] == 0.0 and np.array_equal(u32(got), u32(ref))
+    got0 = gpu_reduce_own(own, np.zeros((0, 8), dtype=np.float32))
+    assert np.array_equal(u32(got0), own.astype(np.uint32) << 16)
+
+
+@pytest.mark.parametrize("wgs,priority", [(1, 0), (3, 3), (1000, 1)])
+def test_reduce_own_knobs_do_not_change_bits(wgs, priority):
+    own = own_bits(70001, seed=5)
+    peers = inputs.reduce_chunks(3, 70001, seed=6).numpy()
+    assert np.array_equal(u32(gpu_reduce_own(own, peers, wgs=wgs, priority=priority)),
+                          u32(oracle.chunk_sum_own_f32(own, peers)))
+
+
+def test_reduce_own_workload_size_bit_exact():
+    # the cb_own share: the 8192 x 8192 GEMM output and 7 fp32 peer chunks
+    from paper_2606_09200_amd.workloads import WORKLOADS
+    w = WORKLOADS["cb_own"]
+    length = w.M * w.N
+    own = torch.randn(length, device=DEV).to(torch.bfloat16)
+    peers = inputs.reduce_chunks(w.nchunks, length, seed=1, device=DEV)
+    out = torch.empty(length, device=DEV)
+    occ.share_reduce_own(own, peers, out)
+    torch.cuda.synchronize()
+    ref = oracle.chunk_sum_own_f32(own.cpu(), peers.cpu().numpy())
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 8, 9, 16, 17, 64])
 @pytest.mark.parametrize("length", [1, 3, 4, 1000, 65539])
 def test_reduce_bit_exact(n, length):

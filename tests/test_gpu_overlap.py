@@ -276,3 +276,44 @@ def test_overlap_tune_with_kn_b_keeps_results():
     assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
     assert np.array_equal(out.cpu().numpy().view(np.uint32),
                           oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
+
+
+@pytest.mark.parametrize("flags", [occ.OCC_RUN_OVL, occ.OCC_RUN_SEQ, occ.OCC_RUN_OVL | occ.OCC_RUN_GRAPH, 0])
+def test_overlap_collective_consumes_each_iterations_gemm_output(flags):
+    # C holds one output per iteration, poisoned with NaN beforehand: every
+    # C_i must be the GEMM's result and the last collective's output the
+    # fixed-order sum of C_{n-1} and the peer chunks, i.e. each collective
+    # read its own iteration's output after that GEMM wrote it
+    n_iter, M, N, K = 4, 520, 264, 136
+    A, B = inputs.gemm_operands(M, N, K, seed=3, device=DEV)
+    C = torch.full((n_iter, M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+    peers = inputs.reduce_chunks(3, M * N, seed=4, device=DEV)
+    out = torch.full((M * N,), float("nan"), device=DEV)
+    C_ref = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm(A, B, C_ref)
+    r = occ.run_overlap(A, B, C, bufs=peers, out=out, reduce_own=True, n_iter=n_iter, reps=1, warmup=0,
+                        flags=flags, comm_priority=0)
+    torch.cuda.synchronize()
+    for i in range(n_iter):
+        assert torch.equal(C[i].view(torch.int16), C_ref.view(torch.int16)), i
+    ref = oracle.chunk_sum_own_f32(C[-1].cpu(), peers.cpu().numpy())
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    if flags & occ.OCC_RUN_OVL or flags == 0:
+        assert r["t_ovl_ms"] > 0
+    if flags & occ.OCC_RUN_SEQ or flags == 0:
+        assert r["t_seq_ms"] > 0
+
+
+def test_overlap_reduce_own_no_peers_and_timeline():
+    n_iter, M, N, K = 3, 256, 256, 512
+    A, B = inputs.gemm_operands(M, N, K, seed=5, device=DEV)
+    C = torch.zeros((n_iter, M, N), device=DEV, dtype=torch.bfloat16)
+    out = torch.empty(M * N, device=DEV)
+    tl = torch.zeros(4 * n_iter, dtype=torch.int64, device=DEV)
+    occ.run_overlap(A, B, C, bufs=None, out=out, reduce_own=True, n_iter=n_iter, reps=1, warmup=0,
+                    flags=occ.OCC_RUN_OVL, timeline=tl)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy().view(np.uint32),
+                          C[-1].view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1).astype(np.uint32) << 16)
+    g, c = timeline_intervals(tl, n_iter)
+    assert schedule.dependency_violations(g, c) == []

@@ -79,5 +79,9 @@ def test_workload_table():
         assert x.gemm_bytes == 2.0 * (x.M * x.K + x.N * x.K + x.M * x.N)
         if x.comm == "reduce":
             assert x.comm_bytes == 4.0 * x.length * (x.nchunks + 1)
+        elif x.comm == "reduce_own":
+            assert x.length == x.M * x.N                  # the collective consumes C_i
+            assert x.comm_bytes == 2.0 * x.length + 4.0 * x.length * (x.nchunks + 1)
         else:
             assert x.comm_bytes == 2.0 * x.nchunks * x.chunk_bytes
+    assert w["cb_own"].comm == "reduce_own" and w["cb_own"].nchunks == 7

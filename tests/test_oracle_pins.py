@@ -233,6 +233,59 @@ def test_chunk_sum_brute_force_binary32():
         assert f32_bits(float(got[j])) == f32_bits(acc), j
 
 
+# ------------------------------------------------ chunk sum with a bf16 own term
+def _widen(u16):
+    """bf16 bit patterns -> float32 by placing them in the high half (exact)."""
+    return (np.asarray(u16, dtype=np.uint32) << 16).view(np.float32)
+
+
+def test_chunk_sum_own_without_peers_is_the_widened_own_term():
+    # every bf16 pattern, no peer chunks: out is the pattern widened, bit for
+    # bit, and its value is the bf16 value (checked through the GEMM's own
+    # bf16 -> double conversion for every non-NaN pattern)
+    own = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = oracle.chunk_sum_own_f32(own, np.zeros((0, own.size), dtype=np.float32))
+    assert np.array_equal(got.view(np.uint32), (own.astype(np.uint32) << 16))
+    for h in range(0, 1 << 16, 97):
+        v = oracle.bf16_to_double(h)
+        if not math.isnan(v):
+            assert float(got[h]) == v, hex(h)
+
+
+def test_chunk_sum_own_order_own_first():
+    # ((1 + 2^24) - 2^24) = 0 in binary32 (1 + 2^24 rounds to 2^24), while any
+    # other grouping or own-last order gives 1: the own term comes first and
+    # the fold is strictly left to right
+    own = np.array([0x3F80], dtype=np.uint16)                      # 1.0
+    peers = np.array([[2.0 ** 24], [-(2.0 ** 24)]], dtype=np.float32)
+    assert oracle.chunk_sum_own_f32(own, peers)[0] == 0.0
+    assert oracle.chunk_sum_f32(np.vstack([peers, [[1.0]]]).astype(np.float32))[0] == 1.0
+
+
+def test_chunk_sum_own_integer_valued_exact_and_equal_to_widened_chunk_sum():
+    rng = np.random.default_rng(6)
+    own_i = rng.integers(-128, 129, size=4000)                     # exact in bf16
+    own = (np.asarray(own_i, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal(_widen(own), own_i.astype(np.float32))
+    peers = rng.integers(-1024, 1025, size=(7, 4000))
+    got = oracle.chunk_sum_own_f32(own, peers.astype(np.float32))
+    assert np.array_equal(got, (own_i + peers.sum(axis=0)).astype(np.float32))
+    # with rounding: the same as the plain chunk sum whose first chunk is the widened own term
+    x = (rng.random((5, 999)) * 2 - 1).astype(np.float32) * np.float32(3.0e4)
+    own2 = (x[0].view(np.uint32) >> 16).astype(np.uint16)
+    ref = oracle.chunk_sum_f32(np.vstack([_widen(own2)[None, :], x[1:]]))
+    assert np.array_equal(oracle.chunk_sum_own_f32(own2, x[1:]).view(np.uint32), ref.view(np.uint32))
+
+
+def test_chunk_sum_own_special_values():
+    own = np.array([0x7F80, 0xFF80, 0x7FC0, 0x0001, 0x8000], dtype=np.uint16)  # inf, -inf, nan, min subnormal, -0
+    peers = np.zeros((1, 5), dtype=np.float32)
+    got = oracle.chunk_sum_own_f32(own, peers)
+    assert np.isposinf(got[0]) and np.isneginf(got[1]) and np.isnan(got[2])
+    assert got[3] == np.float32(2.0 ** -133)
+    assert got[4] == 0.0      # -0 + (+0) = +0 in round-to-nearest
+
+
 # ---------------------------------------------------------------- permutation
 def test_permute_golden():
     rows = {r[0]: r[1] for r in _golden_rows("permute_small.txt")}
