@@ -36,7 +36,7 @@ struct ChunkPtrs {
 // sum is acc = c0[j]; acc = acc + c1[j]; ... exactly in chunk order; the
 // loads of all chunks for UNROLL positions are issued before any addition.
 // Measured on MI355X: for 8 chunks, one position per trip (8 loads in flight
-// per lane, 52 VGPRs) streams 5.3-5.9 TB/s; deeper unrolling adds registers
+// per lane, 38 VGPRs) streams 5.3-5.9 TB/s; deeper unrolling adds registers
 // without adding bandwidth.  The default grid is one workgroup per CU (one
 // wave per SIMD): as fast as two per CU alone, and a co-running GEMM loses
 // less issue time to one comm wave per SIMD than to two.
