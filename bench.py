@@ -241,8 +241,8 @@ def main():
 
     gemm_tflops = w.gemm_flops / (r["t_gemm_ms"] * 1e-3) / 1e12
     comm_gbs = w.comm_bytes / (r["t_comm_ms"] * 1e-3) / 1e9
-    variant = args.variant if args.variant or args.b_layout == "nk" else occ.KN_VARIANTS[0]
-    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, variant, args.gemm_grid)
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, args.variant, args.gemm_grid,
+                                   b_layout=args.b_layout)
     gemm_name = "occ_gemm" if args.b_layout == "nk" else "occ_gemm_kn"
     traffic_key = w.name if args.b_layout == "nk" else w.name + "_kn"
     gemm_bound_mb = w.M <= 16

@@ -107,7 +107,11 @@ enum {
   OCC_GEMM_SKINNY_AREG_K8192 = 28,
   OCC_GEMM_SKINNY_AREG_K4096 = 29,
   /* B stored K x N (occ_gemm_kn / occ_gemm_kn_ex only) */
-  OCC_GEMM_KN_DLP_256x256x64_8W_2ST = 32
+  OCC_GEMM_KN_DLP_256x256x64_8W_2ST = 32,
+  /* skinny (M <= 16) with B stored K x N: 128-column units over the whole K,
+     4 waves splitting K, 32-row blocks of B and A streamed into LDS (2
+     stages); automatic choice for occ_gemm_kn when M <= 16. */
+  OCC_GEMM_KN_SKINNY_4W_2ST = 33
 };
 
 /*
@@ -121,7 +125,7 @@ enum {
  * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
  * an unknown variant, a skinny variant with M > 16, a K that variant 28/29
  * does not take, or K above 4 M for a direct-to-LDS variant with 256-row
- * tiles (8 M with 128-row tiles: variants 10-19, 24-27, 32-38 address an
+ * tiles (8 M with 128-row tiles: variants 10-19, 24-27 and 32 address an
  * operand tile with 32-bit offsets; for such K the automatic choice falls
  * back to a register-staged variant).
  */
@@ -132,8 +136,10 @@ int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size
  * occ_gemm_kn -- C = A * B with B stored K x N (row-major, N-contiguous):
  *   C[m][n] = sum_k A[m][k] * B[k][n].  Same arithmetic, rounding and LDS pad
  * as occ_gemm; the B tile is staged in LDS as stored and its MFMA operands
- * are read with gfx950's LDS transpose reads.  Results are bit-identical to
- * occ_gemm on the transposed B (same order of the k sums).
+ * are read with gfx950's LDS transpose reads.  For M > 16 the results are
+ * bit-identical to occ_gemm's default 256x256 tile on the transposed B (same
+ * order of the k sums); for M <= 16 a skinny kernel (variant 33) splits K
+ * across waves and may differ from it in the last bit.
  * Requirements: as occ_gemm, plus N % 8 == 0 (16-byte B rows), N at most
  * 16 M and K at most 4 M (a k-step of B and a tile of A are addressed with
  * 32-bit offsets; larger is OCC_EINVAL).
@@ -141,9 +147,10 @@ int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size
 int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 void *stream);
 
-/* occ_gemm_kn_ex -- occ_gemm_kn with a variant (0 = automatic, or
-   OCC_GEMM_KN_DLP_256x256x64_8W_2ST) and a grid cap as in occ_gemm_ex.
-   OCC_EINVAL for a variant that reads B as N x K. */
+/* occ_gemm_kn_ex -- occ_gemm_kn with a variant (0 = automatic,
+   OCC_GEMM_KN_DLP_256x256x64_8W_2ST, or OCC_GEMM_KN_SKINNY_4W_2ST for
+   M <= 16) and a grid cap as in occ_gemm_ex.  OCC_EINVAL for a variant that
+   reads B as N x K, or the skinny one with M > 16. */
 int occ_gemm_kn_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                    int variant, int grid_cap, void *stream);
 
@@ -170,6 +177,13 @@ typedef struct occ_gemm_plan {
  */
 int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                         occ_gemm_plan *plan);
+
+/* occ_gemm_kn_plan_query -- the plan for occ_gemm_kn_ex(M, N, K, lds_bytes,
+   variant, grid_cap): as occ_gemm_plan_query, with variant 0 standing for
+   occ_gemm_kn's automatic choice.  OCC_EINVAL for a variant that reads B as
+   N x K. */
+int occ_gemm_kn_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
+                           occ_gemm_plan *plan);
 
 /*
  * occ_gemm_info -- the three LDS figures of Section 3.1 for the kernel used
@@ -383,7 +397,7 @@ const char *occ_strerror(int status);
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
 #define OCC_VERSION_MAJOR 1
-#define OCC_VERSION_MINOR 3
+#define OCC_VERSION_MINOR 4
 int occ_version(void);
 
 #ifdef __cplusplus

@@ -34,9 +34,9 @@ GEMM_VARIANTS = {
     28: "skinny A-in-registers K<=8192", 29: "skinny A-in-registers K<=4096",
     32: "dl+pipe 256x256x64 8w 2st, B K x N",
 }
-KN_VARIANTS = (32,)       # take B stored K x N (occ_gemm_kn_ex only)
+KN_VARIANTS = (32, 33)    # take B stored K x N (occ_gemm_kn_ex only); 33: M <= 16
 SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
-ABI_VERSION = (1, 3)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+ABI_VERSION = (1, 4)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -89,6 +89,8 @@ _SIGS = {
                        ctypes.c_int, ctypes.c_int, _P],
     "occ_gemm_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                             ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
+    "occ_gemm_kn_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
+                               ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
     "occ_gemm_info": [ctypes.POINTER(ctypes.c_int)] * 3,
     "share_reduce": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, _P],
     "share_reduce_ex": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, ctypes.c_int,
@@ -191,13 +193,17 @@ def occ_gemm_kn_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
     return C
 
 
-def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False):
-    """Plan as a dict; 'feasible' is False when the pad does not fit (OCC_ELDS)."""
+def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False, b_layout="nk"):
+    """Plan as a dict; 'feasible' is False when the pad does not fit (OCC_ELDS).
+    b_layout "kn" asks for occ_gemm_kn's plan (occ_gemm_kn_plan_query)."""
+    if b_layout not in ("nk", "kn"):
+        raise ValueError("b_layout must be 'nk' or 'kn'")
+    name = "occ_gemm_kn_plan_query" if b_layout == "kn" else "occ_gemm_plan_query"
     p = occ_gemm_plan()
-    st = lib().occ_gemm_plan_query(int(M), int(N), int(K), int(lds_bytes), int(variant),
-                                   int(grid_cap), ctypes.byref(p))
+    st = getattr(lib(), name)(int(M), int(N), int(K), int(lds_bytes), int(variant), int(grid_cap),
+                              ctypes.byref(p))
     if st not in (OCC_OK, OCC_ELDS) or (strict and st != OCC_OK):
-        raise OccError(st, "occ_gemm_plan_query")
+        raise OccError(st, name)
     d = {f: getattr(p, f) for f, _ in occ_gemm_plan._fields_}
     d["feasible"] = st == OCC_OK
     return d

@@ -144,6 +144,15 @@ int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int 
   return occ::gemm_plan(c, plan);
 }
 
+int occ_gemm_kn_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
+                           occ_gemm_plan *plan) {
+  if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
+  memset(plan, 0, sizeof *plan);
+  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0},
+                  true};
+  return occ::gemm_plan(c, plan);
+}
+
 int occ_gemm_info(int *tile_lds_bytes, int *max_lds_per_wg, int *lds_per_cu) {
   if (tile_lds_bytes == nullptr || max_lds_per_wg == nullptr || lds_per_cu == nullptr) return OCC_EINVAL;
   occ_gemm_plan p;

@@ -10,11 +10,12 @@
 // read from LDS as 16-byte rows), C is M x N, all row-major.
 //
 // The kernels live in gemm_tiled.h (register-staged tiles, the paper's
-// opt1/opt2), gemm_dl.h (direct-to-LDS tiles, the default for large shapes)
-// and gemm_skinny.h (M <= 16); this file holds the variant table, the launch
-// plan and the launcher.
+// opt1/opt2), gemm_dl.h (direct-to-LDS tiles, the default for large shapes),
+// gemm_skinny.h (M <= 16) and gemm_skinny_kn.h (M <= 16, B stored K x N);
+// this file holds the variant table, the launch plan and the launcher.
 #include "gemm_dl.h"
 #include "gemm_skinny.h"
+#include "gemm_skinny_kn.h"
 #include "gemm_tiled.h"
 
 #include <algorithm>
@@ -39,6 +40,7 @@ struct Variant {
   int kmult;         // K must be a multiple of this (0 = any)
   bool b_kn;         // takes B stored K x N (and only that)
   int nmax;          // largest N the kernel takes (0 = any)
+  int per_cu;        // skinny kernels: persistent workgroups per CU (0 = 1)
 };
 
 template <class T>
@@ -78,6 +80,16 @@ constexpr Variant make_skinny_areg_variant(int id, const char *name) {
   return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, 2 * (WAVES - 1) * 64 * 16, nullptr,
                  gemm_skinny_areg_kernel<WAVES, KBW, UNROLL>, name, WAVES * KBW * kSkinnyKB,
                  2 * WAVES * kSkinnyKB * UNROLL, false, 0};
+}
+
+// A K x N B block (32 rows of N) is addressed with 32-bit offsets from its
+// first row (columns past N marked with 2^31), an A row (M <= 16 rows of K)
+// likewise from A.
+template <int WAVES, int STAGES, int COLS>
+constexpr Variant make_skinny_kn_variant(int id, const char *name) {
+  return Variant{id, 16, COLS, kSknKB, 64 * WAVES, SkinnyKn<WAVES, STAGES, COLS>::LDS_BYTES, nullptr,
+                 gemm_skinny_kn_kernel<WAVES, STAGES, COLS>, name, (int)((0x80000000ull / 32u) & ~7ull), 0,
+                 true, (int)((0x80000000ull / (2u * kSknKB)) & ~7ull), 2};
 }
 
 using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
@@ -141,13 +153,15 @@ const Variant kVariants[] = {
     make_skinny_areg_variant<8, 32, 4>(28, "skinny M<=16, A in registers, 8 waves, K<=8192, K%2048==0"),
     make_skinny_areg_variant<8, 16, 4>(29, "skinny M<=16, A in registers, 8 waves, K<=4096, K%2048==0"),
     make_dl_variant<PKN256x256_8w_2s>(32, "dl+pipe 256x256x64 8w 2st, B K x N"),
+    make_skinny_kn_variant<4, 2, 128>(33, "skinny M<=16, B K x N, 128-column units, 4 waves, 2 LDS stages"),
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
 
-constexpr int kKnVariant = 32;  // the K x N B kernel
+constexpr int kKnVariant = 32;        // the K x N B kernel
+constexpr int kKnSkinnyVariant = 33;  // the K x N B kernel for M <= 16
 
 const Variant *find_variant(int id) {
   for (const Variant &v : kVariants)
@@ -194,9 +208,10 @@ static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_g
   p->tile_k = v->bk;
   p->threads = v->threads;
   p->tile_lds_bytes = v->lds;
-  p->tiles = skinny ? ceil_div(c.N, 16) : ceil_div(c.M, v->bm) * ceil_div(c.N, v->bn);
+  p->tiles = skinny ? ceil_div(c.N, v->bn) : ceil_div(c.M, v->bm) * ceil_div(c.N, v->bn);
   p->grid = p->tiles;
-  if (skinny && p->grid > di.num_cus) p->grid = di.num_cus;  // persistent, one per CU
+  const int skinny_grid = di.num_cus * (v->per_cu > 0 ? v->per_cu : 1);
+  if (skinny && p->grid > skinny_grid) p->grid = skinny_grid;  // persistent
   if (c.grid_cap > 0 && c.grid_cap < p->grid) p->grid = c.grid_cap;
   p->max_lds_per_wg = di.max_lds_per_wg;
   p->lds_per_cu = di.lds_per_cu;
@@ -214,7 +229,8 @@ int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
   int st = current_device_info(&di);
   if (st != OCC_OK) return st;
   int variant = c.variant;
-  if (variant == 0) variant = c.b_kn ? kKnVariant : auto_variant(c.M, c.N, c.K, di->num_cus);
+  if (variant == 0)
+    variant = c.b_kn ? (c.M <= 16 ? kKnSkinnyVariant : kKnVariant) : auto_variant(c.M, c.N, c.K, di->num_cus);
   st = fill_plan(c, variant, *di, plan);
   if (st != OCC_OK) return st;
   const Variant *v = find_variant(variant);

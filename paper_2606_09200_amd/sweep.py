@@ -50,10 +50,8 @@ def setup(w, dev):
 
 
 def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs):
-    variant = knobs.get("gemm_variant", 0)
-    if knobs.get("b_layout", "nk") == "kn" and variant == 0:
-        variant = occ.KN_VARIANTS[0]
-    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, variant, knobs.get("gemm_grid", 0))
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0), knobs.get("gemm_grid", 0),
+                                   b_layout=knobs.get("b_layout", "nk"))
     row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
            "gemm_grid": plan["grid"],
            "gemm_variant": plan["kernel_id"], "gemm_tile_lds": plan["tile_lds_bytes"],

@@ -208,6 +208,13 @@ def test_gemm_full_size_skinny_full_parity():
         occ.occ_gemm_ex(A, B, C, variant=v)
         torch.cuda.synchronize()
         assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full, variant %d" % v)
+    # B stored K x N: the skinny K x N kernel (automatic) and the 256x256 tile
+    Bkn = B.t().contiguous()
+    for v in (0, 33, 32):
+        C = torch.full((w.M, w.N), float("nan"), device=DEV, dtype=torch.bfloat16)
+        occ.occ_gemm_kn_ex(A, Bkn, C, variant=v)
+        torch.cuda.synchronize()
+        assert_gemm_close(bf16_bits(C), ref, 1.0, w.std_b, w.K, "mb full, K x N, variant %d" % v)
 
 
 # ------------------------------------------------------------- B stored K x N
@@ -230,8 +237,13 @@ def test_gemm_kn_full_parity(M, N, K):
     got = run_gemm_kn(A, Bkn)
     ref = oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn")
     assert_gemm_close(got, ref, 1.0, 1.0, K, "kn %dx%dx%d" % (M, N, K))
-    # the same tile, MFMA sequence and k order as the N x K kernel: same bits
-    assert np.array_equal(got, run_gemm(A, B, variant=16))
+    if M > 16:
+        # the same tile, MFMA sequence and k order as the N x K kernel: same bits
+        assert np.array_equal(got, run_gemm(A, B, variant=16))
+    else:
+        # the skinny K x N kernel (automatic for M <= 16)
+        assert occ.occ_gemm_plan_query(M, N, K, b_layout="kn")["kernel_id"] == 33
+        assert np.array_equal(got, run_gemm_kn(A, Bkn, variant=33))
 
 
 def test_gemm_kn_integer_bit_exact_and_invariant():
@@ -242,6 +254,56 @@ def test_gemm_kn_integer_bit_exact_and_invariant():
     for cap in (1, 3, 256):
         assert np.array_equal(run_gemm_kn(A, Bkn, grid_cap=cap), base), cap
     assert np.array_equal(run_gemm_kn(A, Bkn, lds_bytes=16 << 10, variant=32), base)
+
+
+@pytest.mark.parametrize("M", [1, 5, 16])
+@pytest.mark.parametrize("N,K", [(8, 8), (136, 40), (1000, 1032), (4104, 4096), (264, 8200), (128, 32)])
+def test_gemm_kn_skinny_full_parity(M, N, K):
+    # ragged N (partial 128-column unit), K not a multiple of the 32-row
+    # block or of the 4-wave split, fewer blocks than waves
+    A, B = inputs.gemm_operands(M, N, K, seed=M + N + K)
+    Bkn = B.t().contiguous()
+    got = run_gemm_kn(A, Bkn, variant=33)
+    ref = oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn")
+    assert_gemm_close(got, ref, 1.0, 1.0, K, "kn skinny %dx%dx%d" % (M, N, K))
+
+
+def test_gemm_kn_skinny_integer_bit_exact_and_invariant():
+    # sums of products of {-2..2} are exact in fp32 in any order
+    A, B = int_operands(13, 1160, 2056, seed=12)
+    Bkn = B.t().contiguous()
+    base = run_gemm_kn(A, Bkn, variant=33)
+    assert np.array_equal(base, oracle.gemm_bf16(A, Bkn, 13, 1160, 2056, b_layout="kn"))
+    for cap in (1, 3, 7):
+        assert np.array_equal(run_gemm_kn(A, Bkn, variant=33, grid_cap=cap), base), cap
+    assert np.array_equal(run_gemm_kn(A, Bkn, variant=33, lds_bytes=64 << 10), base)
+    # a value a k-block past K would change the sum: nothing past K is read
+    A2, B2 = int_operands(16, 256, 48, seed=13)
+    big = torch.cat([B2.t().contiguous(), torch.full((16, 256), 2.0, dtype=torch.bfloat16)])
+    C = torch.full((16, 256), float("nan"), device=DEV, dtype=torch.bfloat16)
+    Ad, Bd = A2.to(DEV), big.to(DEV)                    # B has 64 rows; K = 48 uses 48
+    assert occ.lib().occ_gemm_kn_ex(occ._ptr(Ad), occ._ptr(Bd), occ._ptr(C), 16, 256, 48, 0, 33, 0,
+                                    occ._stream(None)) == occ.OCC_OK
+    torch.cuda.synchronize()
+    assert np.array_equal(bf16_bits(C), oracle.gemm_bf16(A2, B2.t().contiguous(), 16, 256, 48, b_layout="kn"))
+
+
+def test_gemm_kn_skinny_plan_and_checks():
+    p = occ.occ_gemm_plan_query(16, 28672, 8192, b_layout="kn")
+    assert p["kernel_id"] == 33 and p["tile_n"] == 128 and p["tiles"] == 224
+    assert p["grid"] == min(224, 2 * p["num_cus"]) and p["wg_per_cu"] >= 1
+    assert occ.occ_gemm_plan_query(17, 28672, 8192, b_layout="kn")["kernel_id"] == 32
+    assert occ.occ_gemm_plan_query(16, 28672, 8192, 0, 33)["kernel_id"] == 33   # K x N from the id
+    with pytest.raises(occ.OccError):                   # the K x N plan of an N x K variant
+        occ.occ_gemm_plan_query(16, 64, 64, 0, 28, b_layout="kn")
+    A, B = inputs.gemm_operands(17, 64, 64, seed=2, device=DEV)
+    C = torch.empty((17, 64), device=DEV, dtype=torch.bfloat16)
+    with pytest.raises(occ.OccError) as e:              # M > 16
+        occ.occ_gemm_kn_ex(A, B.t().contiguous(), C, variant=33)
+    assert e.value.status == occ.OCC_EINVAL
+    with pytest.raises(occ.OccError) as e:              # B read as N x K
+        occ.occ_gemm_ex(A[:16], B, C[:16], variant=33)
+    assert e.value.status == occ.OCC_EINVAL
 
 
 def test_gemm_kn_layout_checks():
