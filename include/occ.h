@@ -102,10 +102,14 @@ enum {
   OCC_GEMM_DLP_128x256x32_4W_3ST = 27,
   /* skinny (M <= 16) with each wave's K-slice of A held in registers: B is
      the only operand streamed per 16-column unit.  K must be a positive
-     multiple of 2048 and at most 8192 (28) / 4096 (29); automatic choice for
-     such K when M <= 16. */
+     multiple of 2048 and at most 8192 (28) / 4096 (29). */
   OCC_GEMM_SKINNY_AREG_K8192 = 28,
   OCC_GEMM_SKINNY_AREG_K4096 = 29,
+  /* skinny (M <= 16) with A held in registers and B staged through LDS in
+     blocks of 16 rows x 128 k (whole 256-byte row pieces per DMA
+     instruction).  K must be a positive multiple of 1024 and at most 8192;
+     automatic choice for such K when M <= 16. */
+  OCC_GEMM_SKINNY_LDSB_K8192 = 34,
   /* B stored K x N (occ_gemm_kn / occ_gemm_kn_ex only) */
   OCC_GEMM_KN_DLP_256x256x64_8W_2ST = 32,
   /* skinny (M <= 16) with B stored K x N: 128-column units over the whole K,
@@ -121,9 +125,9 @@ enum {
  * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
  * and the pad never change the result.  The tiled variants (1-7, 9-19, 24-27)
  * accumulate every output over k in the same order and give bit-identical
- * results; the skinny variants (8, 20-23, 28, 29) split K across waves and
+ * results; the skinny variants (8, 20-23, 28, 29, 34) split K across waves and
  * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
- * an unknown variant, a skinny variant with M > 16, a K that variant 28/29
+ * an unknown variant, a skinny variant with M > 16, a K that variant 28/29/34
  * does not take, or K above 4 M for a direct-to-LDS variant with 256-row
  * tiles (8 M with 128-row tiles: variants 10-19, 24-27 and 32 address an
  * operand tile with 32-bit offsets; for such K the automatic choice falls

@@ -11,11 +11,13 @@
 //
 // The kernels live in gemm_tiled.h (register-staged tiles, the paper's
 // opt1/opt2), gemm_dl.h (direct-to-LDS tiles, the default for large shapes),
-// gemm_skinny.h (M <= 16) and gemm_skinny_kn.h (M <= 16, B stored K x N);
-// this file holds the variant table, the launch plan and the launcher.
+// gemm_skinny.h and gemm_skinny_ldsb.h (M <= 16) and gemm_skinny_kn.h
+// (M <= 16, B stored K x N); this file holds the variant table, the launch
+// plan and the launcher.
 #include "gemm_dl.h"
 #include "gemm_skinny.h"
 #include "gemm_skinny_kn.h"
+#include "gemm_skinny_ldsb.h"
 #include "gemm_tiled.h"
 
 #include <algorithm>
@@ -92,6 +94,14 @@ constexpr Variant make_skinny_kn_variant(int id, const char *name) {
                  true, (int)((0x80000000ull / (2u * kSknKB)) & ~7ull), 2};
 }
 
+// B staged through LDS in 128-k blocks, A in registers: K a multiple of
+// 128 * WAVES, at most 32 * WAVES * KBW.
+template <int WAVES, int STAGES, int KBW>
+constexpr Variant make_skinny_ldsb_variant(int id, const char *name) {
+  return Variant{id, 16, 16, kSlbKB, 64 * WAVES, SkinnyLdsB<WAVES, STAGES, KBW>::LDS_BYTES, nullptr,
+                 gemm_skinny_ldsb_kernel<WAVES, STAGES, KBW>, name, 32 * WAVES * KBW, kSlbKB * WAVES, false, 0, 1};
+}
+
 using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
 using T256x256_8w = Tile<256, 256, 64, 2, 4, 2>;
 using T256x128_4w = Tile<256, 128, 64, 2, 2, 2>;
@@ -154,6 +164,7 @@ const Variant kVariants[] = {
     make_skinny_areg_variant<8, 16, 4>(29, "skinny M<=16, A in registers, 8 waves, K<=4096, K%2048==0"),
     make_dl_variant<PKN256x256_8w_2s>(32, "dl+pipe 256x256x64 8w 2st, B K x N"),
     make_skinny_kn_variant<4, 2, 128>(33, "skinny M<=16, B K x N, 128-column units, 4 waves, 2 LDS stages"),
+    make_skinny_ldsb_variant<8, 2, 32>(34, "skinny M<=16, B via LDS in 256-byte row pieces, A in registers, 8 waves, K<=8192, K%1024==0"),
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
@@ -173,10 +184,10 @@ int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 int auto_variant(int M, int N, int K, int num_cus) {
   if (M <= 16) {
-    // skinny, 8 waves; A kept in registers when K is whole 2048-wide slices
-    // that fit, else 8 k-blocks of A and B in flight per lane
-    if (K >= 2048 && K % 2048 == 0 && K <= 4096) return 29;
-    if (K >= 2048 && K % 2048 == 0 && K <= 8192) return 28;
+    // skinny, 8 waves; A kept in registers and B staged through LDS when K
+    // is whole 1024-wide slices that fit, else 8 k-blocks of A and B in
+    // flight per lane
+    if (K >= 1024 && K % 1024 == 0 && K <= 8192) return 34;
     return 21;
   }
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);

@@ -13,6 +13,7 @@ pytestmark = pytest.mark.gpu
 TILED = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13, 14, 15, 16, 17, 18, 19, 24, 25, 26, 27]
 SKINNY = [8, 20, 21, 22, 23]
 AREG = {28: 8192, 29: 4096}   # skinny with A in registers: largest K (K % 2048 == 0)
+LDSB = 34                     # skinny, A in registers, B through LDS: K % 1024 == 0, K <= 8192
 
 
 def run_gemm(A, B, lds_bytes=0, variant=0, grid_cap=0):
@@ -92,9 +93,39 @@ def test_gemm_skinny_areg_rejects_unsupported_k(variant):
         assert e.value.status == occ.OCC_EINVAL, K
     with pytest.raises(occ.OccError):
         occ.occ_gemm_plan_query(16, 64, 0, 0, variant)          # K = 0: not this kernel
-    assert occ.occ_gemm_plan_query(16, 64, 4096, 0, 0)["kernel_id"] == 29
-    assert occ.occ_gemm_plan_query(16, 64, 8192, 0, 0)["kernel_id"] == 28
-    assert occ.occ_gemm_plan_query(16, 64, 8200, 0, 0)["kernel_id"] == 21
+    for K, v in ((1024, LDSB), (3072, LDSB), (4096, LDSB), (8192, LDSB), (512, 21), (8200, 21), (9216, 21)):
+        assert occ.occ_gemm_plan_query(16, 64, K, 0, 0)["kernel_id"] == v, K
+
+
+@pytest.mark.parametrize("M,N", [(16, 260), (1, 17), (13, 1000)])
+def test_gemm_skinny_ldsb_full_parity(M, N):
+    for K in (1024, 3072, 8192):
+        A, B = inputs.gemm_operands(M, N, K, seed=M + K)
+        got = run_gemm(A, B, variant=LDSB)
+        ref = oracle.gemm_bf16(A, B, M, N, K)
+        assert_gemm_close(got, ref, 1.0, 1.0, K, "variant %d %dx%dx%d" % (LDSB, M, N, K))
+
+
+def test_gemm_skinny_ldsb_integer_bit_exact_and_invariant():
+    # sums of products of {-2..2} are exact in fp32 in any order; grid caps
+    # make workgroups run several units, so the block stream crosses units
+    A, B = int_operands(11, 1000, 2048, seed=34)
+    base = run_gemm(A, B, variant=LDSB)
+    assert np.array_equal(base, oracle.gemm_bf16(A, B, 11, 1000, 2048))
+    for cap in (1, 3, 7):
+        assert np.array_equal(run_gemm(A, B, variant=LDSB, grid_cap=cap), base), cap
+    assert np.array_equal(run_gemm(A, B, variant=LDSB, lds_bytes=32 << 10), base)
+
+
+def test_gemm_skinny_ldsb_rejects_unsupported_k():
+    for K in (1032, 512, 1536, 9216):
+        A, B = inputs.gemm_operands(16, 64, K, seed=1, device=DEV)
+        C = torch.empty((16, 64), device=DEV, dtype=torch.bfloat16)
+        with pytest.raises(occ.OccError) as e:
+            occ.occ_gemm_ex(A, B, C, variant=LDSB)
+        assert e.value.status == occ.OCC_EINVAL, K
+    with pytest.raises(occ.OccError):
+        occ.occ_gemm_plan_query(16, 64, 0, 0, LDSB)
 
 
 def test_gemm_direct_to_lds_k_limit():
@@ -203,7 +234,7 @@ def test_gemm_full_size_skinny_full_parity():
     w = WORKLOADS["mb"]
     A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=DEV)
     ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), w.M, w.N, w.K)
-    for v in [0] + SKINNY + [28]:
+    for v in [0] + SKINNY + [28, LDSB]:
         C = torch.full((w.M, w.N), float("nan"), device=DEV, dtype=torch.bfloat16)
         occ.occ_gemm_ex(A, B, C, variant=v)
         torch.cuda.synchronize()
