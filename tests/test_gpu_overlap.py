@@ -56,6 +56,38 @@ def test_overlap_results_match_plain_calls(pad, prio):
                           oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
 
 
+@pytest.mark.parametrize("b_layout,variant", [("nk", 34), ("kn", 33)])
+def test_overlap_skinny_gemm_matches_plain_calls_and_traces(b_layout, variant):
+    # decode-like M <= 16: the LDS-staged skinny kernels (automatic choice)
+    # inside both schedules, with every workgroup traced
+    n, M, N, K = 3, 16, 1160, 2048
+    A, B = inputs.gemm_operands(M, N, K, seed=5, device=DEV)
+    Bx = B.t().contiguous() if b_layout == "kn" else B
+    C = torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+    C_ref = torch.empty_like(C)
+    chunks = inputs.reduce_chunks(4, 1 << 20, seed=1, device=DEV)
+    out = torch.empty(1 << 20, device=DEV)
+    (occ.occ_gemm_kn if b_layout == "kn" else occ.occ_gemm)(A, Bx, C_ref)
+    plan = occ.occ_gemm_plan_query(M, N, K, b_layout=b_layout)
+    assert plan["kernel_id"] == variant
+    cap = 4096
+    wt = torch.zeros(4 + occ.WG_RECORD_WORDS * cap, dtype=torch.int32, device=DEV)
+    r = occ.run_overlap(A, Bx, C, bufs=chunks, out=out, b_layout=b_layout, comm_priority=0, n_iter=n,
+                        reps=1, warmup=0, comm_wgs=32, wg_trace=wt)
+    torch.cuda.synchronize()
+    assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(Bx), M, N, K, b_layout=b_layout)
+    assert_gemm_close(bf16_bits(C), ref, 1.0, 1.0, K, "overlap skinny %s C" % b_layout)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32),
+                          oracle.chunk_sum_f32(chunks.cpu().numpy()).view(np.uint32))
+    assert r["t_seq_ms"] > 0 and r["t_ovl_ms"] > 0
+    recs = occ.decode_wg_trace(wt)
+    assert int(wt[0]) == n * (plan["grid"] + 32) <= cap
+    for i in range(n):
+        g = [x for x in recs if x["tag"] == 2 * i]
+        assert sorted(x["block"] for x in g) == list(range(plan["grid"]))
+
+
 def test_overlap_permute_results_match_plain_calls():
     A, B = inputs.gemm_operands(1024, 768, 512, seed=0, device=DEV)
     C = torch.empty((1024, 768), device=DEV, dtype=torch.bfloat16)
