@@ -83,7 +83,7 @@ enum {
   OCC_GEMM_DL_256x256x32_8W_4ST = 11,
   OCC_GEMM_DL_256x256x32_8W_3ST = 12,
   OCC_GEMM_DL_256x128x64_4W_3ST = 13,
-  OCC_GEMM_DL_128x128x64_4W_3ST = 14,
+  OCC_GEMM_DL_128x128x64_4W_3ST = 14,  /* default for mid-size shapes */
   OCC_GEMM_DL_256x128x64_8W_3ST = 15,
   /* direct-to-LDS with LDS-read / MFMA interleaving (16: default for large shapes) */
   OCC_GEMM_DLP_256x256x64_8W_2ST = 16,

@@ -193,7 +193,8 @@ int auto_variant(int M, int N, int K, int num_cus) {
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
   if (big >= num_cus) return K <= find_variant(16)->kmax ? 16 : 3;  // 3: 64-bit addressing
   long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
-  if (mid >= num_cus / 2) return 5;
+  // 128x128 tiles through three direct-to-LDS stages (5: 64-bit addressing)
+  if (mid >= num_cus / 2) return K <= find_variant(14)->kmax ? 14 : 5;
   return 7;
 }
 
