@@ -35,11 +35,13 @@ struct ChunkPtrs {
 // Vector path: all chunk pointers and out are 16-byte aligned.  Element j's
 // sum is acc = c0[j]; acc = acc + c1[j]; ... exactly in chunk order; the
 // loads of all chunks for UNROLL positions are issued before any addition.
-// Measured on MI355X: for 8 chunks, one position per trip (8 loads in flight
-// per lane, 38 VGPRs) streams 5.3-5.9 TB/s; deeper unrolling adds registers
-// without adding bandwidth.  The default grid is one workgroup per CU (one
-// wave per SIMD): as fast as two per CU alone, and a co-running GEMM loses
-// less issue time to one comm wave per SIMD than to two.
+// Measured on MI355X: for 8 terms, two positions per trip (16 loads in
+// flight per lane, 64 VGPRs) stream as fast as one in the isolated pass and
+// make the overlapped 8192^3 schedule 1-2 % shorter (the own-term reduce
+// 6 % faster); four positions fall in between.  The default grid is one
+// workgroup per CU (one wave per SIMD): as fast as two per CU alone, and a
+// co-running GEMM loses less issue time to one comm wave per SIMD than to
+// two.
 //
 // OWN: the first term is a bf16 buffer (this GPU's own contribution, e.g. its
 // GEMM output), widened exactly to binary32; the NC (or nchunks) fp32 chunks
@@ -226,6 +228,11 @@ int clamp_wgs(size_t work_units, int wanted) {
   return (int)(wanted < (long long)cap ? wanted : cap);
 }
 
+// Positions per lane per trip of the vector chunk sum for a number of terms
+// (fp32 chunks plus the own term); the launch table and the pacing period
+// both take it from here.
+constexpr int reduce_unroll(int terms) { return terms == 2 ? 4 : (terms == 4 || terms == 8) ? 2 : 1; }
+
 // Period (10 ns ticks) between a wave's trips so that the whole grid moves
 // trip_bytes per period, i.e. streams at rate_gbs; 0 = unpaced.
 uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
@@ -243,10 +250,10 @@ void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_
                    const uint16_t *own, int prio, uint32_t pace, const KTrace &tr) {
   // instantiations by the number of terms (own + fp32 chunks)
   switch (nchunks + (OWN ? 1 : 0)) {
-    case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, 4, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 4: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 3 : 4, 2, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 8: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 7 : 8, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 16: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 15 : 16, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, reduce_unroll(2), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 4: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 3 : 4, reduce_unroll(4), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 8: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 7 : 8, reduce_unroll(8), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 16: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 15 : 16, reduce_unroll(16), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
     default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
   }
 }
@@ -276,7 +283,7 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
       // positions per lane per trip of each instantiation, and the bytes
       // one position moves
       const int terms = c.nchunks + (own ? 1 : 0);
-      const int unroll = terms == 2 ? 4 : terms == 4 ? 2 : 1;
+      const int unroll = reduce_unroll(terms);
       const double pos_bytes = 16.0 * (c.nchunks + 1) + (own ? 8.0 : 0.0);
       const uint32_t pace = pace_ticks((double)g * kThreads * unroll * pos_bytes, c.rate_gbs);
       // 32-bit offsets when the largest byte offset the loop can form, (nvec
