@@ -233,6 +233,11 @@ int clamp_wgs(size_t work_units, int wanted) {
 // both take it from here.
 constexpr int reduce_unroll(int terms) { return terms == 2 ? 4 : (terms == 4 || terms == 8) ? 2 : 1; }
 
+// Loads in flight per lane of the vector permutation (launch and pacing).
+// 2 and 8 gave no shorter overlapped schedule than 4 (16384x14336x4096 with
+// 64 x 4 MiB, 8192^3 with 4 x 224 MiB).
+constexpr int kPermuteUnroll = 4;
+
 // Period (10 ns ticks) between a wave's trips so that the whole grid moves
 // trip_bytes per period, i.e. streams at rate_gbs; 0 = unpaced.
 uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
@@ -334,14 +339,14 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     int parts = permute_parts(c.chunk_bytes);
     long long items = (long long)c.nchunks * parts;
     int g = (int)(wgs < items ? wgs : items);
-    const uint32_t pace = pace_ticks((double)g * kThreads * 4 * 16.0 * 2.0, c.rate_gbs);
+    const uint32_t pace = pace_ticks((double)g * kThreads * kPermuteUnroll * 16.0 * 2.0, c.rate_gbs);
     // 32-bit offsets when a chunk plus one unrolled block stays below 2^32 bytes
     if ((double)c.chunk_bytes + 4.0 * kThreads * 16.0 < 4294967296.0)
-      hipLaunchKernelGGL((permute_vec_kernel<4, true>), dim3(g), dim3(kThreads), 0, s,
+      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, true>), dim3(g), dim3(kThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
                          c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
     else
-      hipLaunchKernelGGL((permute_vec_kernel<4, false>), dim3(g), dim3(kThreads), 0, s,
+      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, false>), dim3(g), dim3(kThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
                          c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
   } else {
