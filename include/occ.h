@@ -216,7 +216,8 @@ int share_reduce(const float *const *bufs, int nchunks, size_t len, float *out, 
 
 /*
  * share_reduce_ex -- share_reduce with the comm-kernel knobs: `wgs`
- * workgroups (0 = library default: one per CU, fewer for short inputs) and
+ * workgroups of 128 threads (0 = library default: one per CU, fewer for
+ * short inputs) and
  * wave priority `priority` in 0..3
  * (s_setprio; 0 = normal).  Same result for every wgs and priority.
  */
@@ -255,7 +256,8 @@ int share_permute(const void *src, void *dst, const int32_t *perm, int nchunks, 
 int share_reduce_own(const void *own, const float *const *peers, int npeers, size_t len, float *out,
                      int wgs, int priority, void *stream);
 
-/* share_permute_ex -- share_permute with `wgs` and `priority` as share_reduce_ex. */
+/* share_permute_ex -- share_permute with `wgs` (workgroups of 256 threads)
+ * and `priority` as share_reduce_ex. */
 int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes, int wgs, int priority, void *stream);
 

@@ -26,7 +26,17 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // bf16 bit pattern -> binary32 (exact: the bf16 bits are the high half)
 __device__ __forceinline__ float widen_bf16(uint32_t bits16) { return __builtin_bit_cast(float, bits16 << 16); }
 
-constexpr int kThreads = 256;
+// Workgroup sizes.  The chunk sum runs two waves per workgroup: at the
+// default grid of one workgroup per CU, two of a CU's four SIMDs carry a comm
+// wave.  Measured on MI355X against four waves per workgroup: the isolated
+// 8-term sum is 8 % faster, and the overlapped schedules are 1.5-8 % shorter
+// (8192^3 with 8 x 128 MiB, the same with the own term, and 16 x 28672 x 8192
+// with 8 x 28 MiB, at both comm priorities); one wave per workgroup slows the
+// isolated sum by 40 % and lengthens the decode-like schedule.  The
+// permutation keeps four waves: two gave the same overlapped makespan and a
+// 14 % slower isolated copy.
+constexpr int kReduceThreads = 128;
+constexpr int kPermuteThreads = 256;
 
 struct ChunkPtrs {
   const float *p[kMaxReduceChunks];
@@ -39,18 +49,16 @@ struct ChunkPtrs {
 // flight per lane, 64 VGPRs) stream as fast as one in the isolated pass and
 // make the overlapped 8192^3 schedule 1-2 % shorter (the own-term reduce
 // 6 % faster); four positions fall in between.  The default grid is one
-// workgroup per CU (one wave per SIMD): as fast as two per CU alone, and a
-// co-running GEMM loses less issue time to one comm wave per SIMD than to
-// two.
+// workgroup per CU.
 //
 // OWN: the first term is a bf16 buffer (this GPU's own contribution, e.g. its
 // GEMM output), widened exactly to binary32; the NC (or nchunks) fp32 chunks
 // follow it in order.  Its 8 bytes per position are one load.
 template <int NC, int UNROLL, bool OFF32, bool OWN>
-__global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
-                                                              float *__restrict__ out,
-                                                              const uint16_t *__restrict__ own, int prio,
-                                                              uint32_t pace, KTrace tr) {
+__global__ __launch_bounds__(kReduceThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
+                                                                    float *__restrict__ out,
+                                                                    const uint16_t *__restrict__ own, int prio,
+                                                                    uint32_t pace, KTrace tr) {
   // OFF32: every byte offset the loop forms fits in 32 bits (checked by the
   // host), so each access is a scalar base plus one shared 32-bit lane
   // offset instead of a 64-bit address per chunk: fewer vector instructions
@@ -61,8 +69,8 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
   Pacer pc = pace_start(pace);
   const int nc = NC > 0 ? NC : nchunks;
   const I n = (I)nvec;
-  const I stride = (I)gridDim.x * kThreads;
-  I i = (I)blockIdx.x * kThreads + threadIdx.x;
+  const I stride = (I)gridDim.x * kReduceThreads;
+  I i = (I)blockIdx.x * kReduceThreads + threadIdx.x;
   auto ld = [&](int c, I k) {
     return __builtin_nontemporal_load(
         reinterpret_cast<const f32x4 *>(reinterpret_cast<const char *>(cp.p[c]) + k * (I)sizeof(f32x4)));
@@ -134,15 +142,15 @@ __global__ __launch_bounds__(kThreads) void reduce_vec_kernel(ChunkPtrs cp, int 
 
 // Scalar path: elements [first, len) one at a time (the tail after the vector
 // path, or everything when a buffer is not 16-byte aligned).
-__global__ __launch_bounds__(kThreads) void reduce_scalar_kernel(ChunkPtrs cp, int nchunks,
-                                                                 size_t first, size_t len,
-                                                                 float *__restrict__ out,
-                                                                 const uint16_t *__restrict__ own,
-                                                                 int prio, KTrace tr) {
+__global__ __launch_bounds__(kReduceThreads) void reduce_scalar_kernel(ChunkPtrs cp, int nchunks,
+                                                                       size_t first, size_t len,
+                                                                       float *__restrict__ out,
+                                                                       const uint16_t *__restrict__ own,
+                                                                       int prio, KTrace tr) {
   set_wave_priority(prio);
   const TraceStart t0 = trace_begin(tr);
-  const size_t stride = (size_t)gridDim.x * kThreads;
-  for (size_t j = first + (size_t)blockIdx.x * kThreads + threadIdx.x; j < len; j += stride) {
+  const size_t stride = (size_t)gridDim.x * kReduceThreads;
+  for (size_t j = first + (size_t)blockIdx.x * kReduceThreads + threadIdx.x; j < len; j += stride) {
     float acc = own != nullptr ? widen_bf16(own[j]) : cp.p[0][j];
     for (int c = own != nullptr ? 0 : 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
     out[j] = acc;
@@ -158,10 +166,10 @@ struct PermTable {
 // destination chunk (w / parts); workgroups stride over work items, threads
 // over the part's units with UNROLL loads in flight before the stores.
 template <int UNROLL, bool OFF32>
-__global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
-                                                               u32x4 *__restrict__ dst, PermTable pt,
-                                                               int nchunks, size_t cvec, int parts,
-                                                               int prio, uint32_t pace, KTrace tr) {
+__global__ __launch_bounds__(kPermuteThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
+                                                                      u32x4 *__restrict__ dst, PermTable pt,
+                                                                      int nchunks, size_t cvec, int parts,
+                                                                      int prio, uint32_t pace, KTrace tr) {
   // OFF32: offsets inside a chunk fit in 32 bits (checked by the host): the
   // work item's chunk bases are scalar and the lanes share one 32-bit offset.
   using I = typename std::conditional<OFF32, uint32_t, size_t>::type;
@@ -180,33 +188,33 @@ __global__ __launch_bounds__(kThreads) void permute_vec_kernel(const u32x4 *__re
     auto at = [](const char *b, I k) { return reinterpret_cast<const u32x4 *>(b + k * (I)sizeof(u32x4)); };
     auto atw = [](char *b, I k) { return reinterpret_cast<u32x4 *>(b + k * (I)sizeof(u32x4)); };
     I i = lo + threadIdx.x;
-    for (; i + (UNROLL - 1) * kThreads < hi; i += UNROLL * kThreads) {
+    for (; i + (UNROLL - 1) * kPermuteThreads < hi; i += UNROLL * kPermuteThreads) {
       if (!first) pace_wait(pc);
       first = false;
       u32x4 v[UNROLL];
 #pragma unroll
-      for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(at(s, i + u * kThreads));
+      for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(at(s, i + u * kPermuteThreads));
 #pragma unroll
-      for (int u = 0; u < UNROLL; ++u) __builtin_nontemporal_store(v[u], atw(d, i + u * kThreads));
+      for (int u = 0; u < UNROLL; ++u) __builtin_nontemporal_store(v[u], atw(d, i + u * kPermuteThreads));
     }
-    for (; i < hi; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(at(s, i)), atw(d, i));
+    for (; i < hi; i += kPermuteThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(at(s, i)), atw(d, i));
   }
   trace_end(tr, t0);
 }
 
 // Byte path for unaligned buffers or chunk sizes.
-__global__ __launch_bounds__(kThreads) void permute_byte_kernel(const uint8_t *__restrict__ src,
-                                                                uint8_t *__restrict__ dst,
-                                                                PermTable pt, int nchunks,
-                                                                size_t chunk_bytes, int prio,
-                                                                KTrace tr) {
+__global__ __launch_bounds__(kPermuteThreads) void permute_byte_kernel(const uint8_t *__restrict__ src,
+                                                                       uint8_t *__restrict__ dst,
+                                                                       PermTable pt, int nchunks,
+                                                                       size_t chunk_bytes, int prio,
+                                                                       KTrace tr) {
   set_wave_priority(prio);
   const TraceStart t0 = trace_begin(tr);
-  const size_t stride = (size_t)gridDim.x * kThreads;
+  const size_t stride = (size_t)gridDim.x * kPermuteThreads;
   for (int c = 0; c < nchunks; ++c) {
     const uint8_t *s = src + (size_t)pt.p[c] * chunk_bytes;
     uint8_t *d = dst + (size_t)c * chunk_bytes;
-    for (size_t b = (size_t)blockIdx.x * kThreads + threadIdx.x; b < chunk_bytes; b += stride) d[b] = s[b];
+    for (size_t b = (size_t)blockIdx.x * kPermuteThreads + threadIdx.x; b < chunk_bytes; b += stride) d[b] = s[b];
   }
   trace_end(tr, t0);
 }
@@ -222,8 +230,9 @@ __global__ void stamps_reset_kernel(uint64_t *stamps, int npairs, uint32_t *wg) 
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-int clamp_wgs(size_t work_units, int wanted) {
-  size_t cap = (work_units + kThreads - 1) / kThreads;
+// At most one workgroup per `threads` work units, at least one.
+int clamp_wgs(size_t work_units, int wanted, int threads) {
+  size_t cap = (work_units + threads - 1) / threads;
   if (cap < 1) cap = 1;
   return (int)(wanted < (long long)cap ? wanted : cap);
 }
@@ -255,18 +264,18 @@ void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_
                    const uint16_t *own, int prio, uint32_t pace, const KTrace &tr) {
   // instantiations by the number of terms (own + fp32 chunks)
   switch (nchunks + (OWN ? 1 : 0)) {
-    case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, reduce_unroll(2), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 4: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 3 : 4, reduce_unroll(4), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 8: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 7 : 8, reduce_unroll(8), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    case 16: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 15 : 16, reduce_unroll(16), OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
-    default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32, OWN>), dim3(g), dim3(kThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, reduce_unroll(2), OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 4: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 3 : 4, reduce_unroll(4), OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 8: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 7 : 8, reduce_unroll(8), OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    case 16: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 15 : 16, reduce_unroll(16), OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
+    default: hipLaunchKernelGGL((reduce_vec_kernel<0, 1, OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
   }
 }
 
 int reduce_default_wgs(const ReduceCall &c) {
   const DeviceInfo *di = nullptr;
   int cus = current_device_info(&di) == OCC_OK ? di->num_cus : 256;
-  return clamp_wgs(c.len / 4 + 1, cus);
+  return clamp_wgs(c.len / 4 + 1, cus, kReduceThreads);
 }
 
 int reduce_launch(const ReduceCall &c, hipStream_t s) {
@@ -284,16 +293,16 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
   if (vec) {
     size_t nvec = c.len / 4;
     if (nvec > 0) {
-      int g = clamp_wgs(nvec, wgs);
+      int g = clamp_wgs(nvec, wgs, kReduceThreads);
       // positions per lane per trip of each instantiation, and the bytes
       // one position moves
       const int terms = c.nchunks + (own ? 1 : 0);
       const int unroll = reduce_unroll(terms);
       const double pos_bytes = 16.0 * (c.nchunks + 1) + (own ? 8.0 : 0.0);
-      const uint32_t pace = pace_ticks((double)g * kThreads * unroll * pos_bytes, c.rate_gbs);
+      const uint32_t pace = pace_ticks((double)g * kReduceThreads * unroll * pos_bytes, c.rate_gbs);
       // 32-bit offsets when the largest byte offset the loop can form, (nvec
       // plus one unrolled grid stride) * 16, stays below 2^32
-      const bool off32 = ((double)nvec + 4.0 * g * kThreads) * 16.0 < 4294967296.0;
+      const bool off32 = ((double)nvec + 4.0 * g * kReduceThreads) * 16.0 < 4294967296.0;
       if (own) {
         if (off32) launch_reduce<true, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
         else launch_reduce<false, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
@@ -304,10 +313,10 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
     }
     size_t first = nvec * 4;
     if (first < c.len)
-      hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kThreads), 0, s, cp, c.nchunks, first,
+      hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kReduceThreads), 0, s, cp, c.nchunks, first,
                          c.len, c.out, c.own, prio, c.trace);
   } else {
-    hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs)), dim3(kThreads), 0, s, cp,
+    hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs, kReduceThreads)), dim3(kReduceThreads), 0, s, cp,
                        c.nchunks, (size_t)0, c.len, c.out, c.own, prio, c.trace);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
@@ -339,19 +348,19 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     int parts = permute_parts(c.chunk_bytes);
     long long items = (long long)c.nchunks * parts;
     int g = (int)(wgs < items ? wgs : items);
-    const uint32_t pace = pace_ticks((double)g * kThreads * kPermuteUnroll * 16.0 * 2.0, c.rate_gbs);
+    const uint32_t pace = pace_ticks((double)g * kPermuteThreads * kPermuteUnroll * 16.0 * 2.0, c.rate_gbs);
     // 32-bit offsets when a chunk plus one unrolled block stays below 2^32 bytes
-    if ((double)c.chunk_bytes + 4.0 * kThreads * 16.0 < 4294967296.0)
-      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, true>), dim3(g), dim3(kThreads), 0, s,
+    if ((double)c.chunk_bytes + 4.0 * kPermuteThreads * 16.0 < 4294967296.0)
+      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, true>), dim3(g), dim3(kPermuteThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
                          c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
     else
-      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, false>), dim3(g), dim3(kThreads), 0, s,
+      hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, false>), dim3(g), dim3(kPermuteThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
                          c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
   } else {
-    int g = clamp_wgs(c.chunk_bytes, wgs);
-    hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kThreads), 0, s,
+    int g = clamp_wgs(c.chunk_bytes, wgs, kPermuteThreads);
+    hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kPermuteThreads), 0, s,
                        static_cast<const uint8_t *>(c.src), static_cast<uint8_t *>(c.dst), pt,
                        c.nchunks, c.chunk_bytes, c.priority, c.trace);
   }
