@@ -256,7 +256,7 @@ int share_permute(const void *src, void *dst, const int32_t *perm, int nchunks, 
 int share_reduce_own(const void *own, const float *const *peers, int npeers, size_t len, float *out,
                      int wgs, int priority, void *stream);
 
-/* share_permute_ex -- share_permute with `wgs` (workgroups of 256 threads)
+/* share_permute_ex -- share_permute with `wgs` (workgroups of 128 threads)
  * and `priority` as share_reduce_ex. */
 int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunks,
                      size_t chunk_bytes, int wgs, int priority, void *stream);

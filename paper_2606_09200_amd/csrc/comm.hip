@@ -33,10 +33,12 @@ __device__ __forceinline__ float widen_bf16(uint32_t bits16) { return __builtin_
 // (8192^3 with 8 x 128 MiB, the same with the own term, and 16 x 28672 x 8192
 // with 8 x 28 MiB, at both comm priorities); one wave per workgroup slows the
 // isolated sum by 40 % and lengthens the decode-like schedule.  The
-// permutation keeps four waves: two gave the same overlapped makespan and a
-// 14 % slower isolated copy.
+// permutation also runs two waves, with twice the loads in flight per lane
+// of a four-wave workgroup (kPermuteUnroll): against four waves it is 0.5-1 %
+// faster alone and never slower overlapped (8192^3 with 4 x 224 MiB: 0.3-0.9 %
+// shorter).
 constexpr int kReduceThreads = 128;
-constexpr int kPermuteThreads = 256;
+constexpr int kPermuteThreads = 128;
 
 struct ChunkPtrs {
   const float *p[kMaxReduceChunks];
@@ -242,10 +244,11 @@ int clamp_wgs(size_t work_units, int wanted, int threads) {
 // both take it from here.
 constexpr int reduce_unroll(int terms) { return terms == 2 ? 4 : (terms == 4 || terms == 8) ? 2 : 1; }
 
-// Loads in flight per lane of the vector permutation (launch and pacing).
-// 2 and 8 gave no shorter overlapped schedule than 4 (16384x14336x4096 with
-// 64 x 4 MiB, 8192^3 with 4 x 224 MiB).
-constexpr int kPermuteUnroll = 4;
+// Loads in flight per lane of the vector permutation (launch, pacing and the
+// 32-bit offset check).  With four-wave workgroups 2 and 8 gave no shorter
+// overlapped schedule than 4 (16384x14336x4096 with 64 x 4 MiB, 8192^3 with
+// 4 x 224 MiB); the two-wave workgroups take 8, the same bytes per CU.
+constexpr int kPermuteUnroll = 8;
 
 // Period (10 ns ticks) between a wave's trips so that the whole grid moves
 // trip_bytes per period, i.e. streams at rate_gbs; 0 = unpaced.
@@ -350,7 +353,7 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
     int g = (int)(wgs < items ? wgs : items);
     const uint32_t pace = pace_ticks((double)g * kPermuteThreads * kPermuteUnroll * 16.0 * 2.0, c.rate_gbs);
     // 32-bit offsets when a chunk plus one unrolled block stays below 2^32 bytes
-    if ((double)c.chunk_bytes + 4.0 * kPermuteThreads * 16.0 < 4294967296.0)
+    if ((double)c.chunk_bytes + (double)kPermuteUnroll * kPermuteThreads * 16.0 < 4294967296.0)
       hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, true>), dim3(g), dim3(kPermuteThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
                          c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
