@@ -185,7 +185,11 @@ def gpu_permute(src_host, perm, chunk_bytes, byte_offset=0, wgs=0, priority=0):
     return d[byte_offset:byte_offset + total].cpu().numpy()
 
 
-@pytest.mark.parametrize("n,cb", [(1, 16), (4, 4096), (64, 65536), (7, 1040), (512, 48), (3, 1001), (5, 17)])
+# 16 * (3 * 1024 + 517): three full unrolled trips of a 128-lane workgroup
+# and a ragged tail; 16 * (2 * 16384 + 123): one chunk split into three work
+# items of unequal length.
+@pytest.mark.parametrize("n,cb", [(1, 16), (4, 4096), (64, 65536), (7, 1040), (512, 48), (3, 1001), (5, 17),
+                                  (3, 16 * (3 * 1024 + 517)), (2, 16 * (2 * 16384 + 123))])
 def test_permute_bit_exact(n, cb):
     src = inputs.permute_payload(n, cb, seed=n + cb).numpy()
     perm = inputs.chunk_permutation(n, seed=n)
