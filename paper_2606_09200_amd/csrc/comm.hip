@@ -31,7 +31,7 @@ __device__ __forceinline__ float widen_bf16(uint32_t bits16) { return __builtin_
 // wave.  Measured on MI355X against four waves per workgroup: the isolated
 // 8-term sum is 8 % faster, and the overlapped schedules are 1.5-8 % shorter
 // (8192^3 with 8 x 128 MiB, the same with the own term, and 16 x 28672 x 8192
-// with 8 x 28 MiB, at both comm priorities); one wave per workgroup slows the
+// with 8 x 64 MiB, at both comm priorities); one wave per workgroup slows the
 // isolated sum by 40 % and lengthens the decode-like schedule.  The
 // permutation also runs two waves, with twice the loads in flight per lane
 // of a four-wave workgroup (kPermuteUnroll): against four waves it is 0.5-1 %
