@@ -6,8 +6,8 @@
  * per-workgroup LDS footprint shapes its occupancy (Section 3.1), run
  * concurrently with one GPU's local share of a collective K_c (Background,
  * item 2) on a second stream, with the per-iteration dependency
- * K_g^i -> K_c^i enforced by an event (Section 3.2) and the collective given
- * precedence over later GEMMs (Section 3.3).
+ * K_g^i -> K_c^i enforced by an event or a device-side counter (Section 3.2)
+ * and the collective given precedence over later GEMMs (Section 3.3).
  *
  * Conventions for every entry point:
  *   - Device buffers are plain device pointers owned by the caller; the
@@ -37,125 +37,94 @@ typedef enum occ_status {
   OCC_EPERM = -3,   /* perm is not a bijection of [0, nchunks) */
   OCC_EALIAS = -4,  /* an output range overlaps an input range */
   OCC_EHIP = -5,    /* the HIP runtime reported an error (launch, event, stream) */
-  OCC_ENODEV = -6   /* no gfx950 device is current */
+  OCC_ENODEV = -6,  /* no gfx950 device is current */
+  OCC_ETIMEOUT = -7 /* a collective's bounded wait for its GEMM ran out (OCC_DEP_COUNTER) */
 } occ_status;
 
 /* ------------------------------------------------------------------ K_g */
 
 /*
- * occ_gemm -- C = A * op(B), bf16 inputs, fp32 accumulation, bf16 output.
+ * occ_gemm -- C = A * B, bf16 inputs, fp32 accumulation, bf16 output.
  * Background, item 1 (C = alpha op(A) op(B) + beta C) with alpha = 1,
- * beta = 0 (C is overwritten, never read) and op(B) = B^T:
+ * beta = 0 (C is overwritten, never read) and op = identity:
  *   A : M x K, row-major bf16 (uint16 bit patterns), lda = K.
- *   B : N x K, row-major bf16 -- the weight layout of a linear layer, so
- *       C[m][n] = sum_k A[m][k] * B[n][k].
+ *   B : K x N, row-major bf16, ldb = N:  C[m][n] = sum_k A[m][k] * B[k][n].
  *   C : M x N, row-major bf16, ldc = N.  Rounded to nearest-even from fp32.
  * lds_bytes is the EXTRA dynamic LDS each GEMM workgroup reserves on top of
  * the LDS its tile uses (S_tile).  It is never touched; it only lowers the
  * number of GEMM workgroups that fit on a CU (Section 3.1, S_blk).
- * Requirements: M, N, K >= 0; K % 8 == 0; A, B, C 16-byte aligned;
- * C must not overlap A or B.  M == 0 or N == 0 is a no-op; K == 0 writes
- * zeros.  Returns OCC_ELDS if S_tile + lds_bytes exceeds the device's
- * per-workgroup LDS limit (never clamps).
+ * Requirements: M, N, K >= 0; K % 8 == 0 and N % 8 == 0 (16-byte rows);
+ * A, B, C 16-byte aligned; C must not overlap A or B; K at most 4 M and N at
+ * most 16 M (an operand tile is addressed with 32-bit offsets; larger is
+ * OCC_EINVAL).  M == 0 or N == 0 is a no-op; K == 0 writes zeros.  Returns
+ * OCC_ELDS if S_tile + lds_bytes exceeds the device's per-workgroup LDS
+ * limit (never clamps).
  */
 int occ_gemm(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
              void *stream);
 
 /*
  * Kernel variants (tile_m x tile_n x tile_k, waves, LDS stages).  Variant 0
- * lets the library choose from the shape.  6 and 7 are the paper's tile
- * configurations opt1 (64x64x32) and opt2 (64x64x64) of Table 1, with one LDS
- * stage so that S_tile = 2*(TILE_M*TILE_K + TILE_K*TILE_N) bytes (Section 3.1).
+ * lets the library choose from the shape.  Each variant reads B in one
+ * layout: occ_gemm / occ_gemm_ex take the K x N ones, occ_gemm_bt /
+ * occ_gemm_bt_ex the N x K ones.  36/37 (K x N) and 6/7 (N x K) are the
+ * paper's tile configurations opt1 (64x64x32) and opt2 (64x64x64) of Table 1,
+ * with one LDS stage so that S_tile = 2*(TILE_M*TILE_K + TILE_K*TILE_N) bytes
+ * (Section 3.1).
  */
 enum {
   OCC_GEMM_AUTO = 0,
-  OCC_GEMM_256x256x64_4W = 1,
-  OCC_GEMM_256x256x64_8W = 2,
-  OCC_GEMM_256x128x64_4W = 3,
-  OCC_GEMM_256x128x64_4W_1STAGE = 4,
-  OCC_GEMM_128x128x64_4W = 5,
-  OCC_GEMM_OPT1_64x64x32 = 6,
-  OCC_GEMM_OPT2_64x64x64 = 7,
-  OCC_GEMM_SKINNY_M16 = 8,   /* M <= 16 only (4 waves, 16 k-blocks in flight) */
-  OCC_GEMM_256x256x32_4W_1STAGE = 9,
-  /* direct global->LDS variants (buffer_load ... lds, no staging registers) */
-  OCC_GEMM_DL_256x256x64_8W_2ST = 10,
-  OCC_GEMM_DL_256x256x32_8W_4ST = 11,
-  OCC_GEMM_DL_256x256x32_8W_3ST = 12,
-  OCC_GEMM_DL_256x128x64_4W_3ST = 13,
-  OCC_GEMM_DL_128x128x64_4W_3ST = 14,  /* default for mid-size shapes */
-  OCC_GEMM_DL_256x128x64_8W_3ST = 15,
-  /* direct-to-LDS with LDS-read / MFMA interleaving (16: default for large shapes) */
-  OCC_GEMM_DLP_256x256x64_8W_2ST = 16,
-  OCC_GEMM_DLP_256x256x32_8W_4ST = 17,
-  OCC_GEMM_DLP_256x128x64_4W_3ST = 18,
-  OCC_GEMM_DLP_256x256x64_4W_2ST = 19,
-  /* more skinny (M <= 16) variants: waves per workgroup, k-blocks in flight */
-  OCC_GEMM_SKINNY_8W_U16 = 20,
-  OCC_GEMM_SKINNY_8W_U8 = 21,
-  OCC_GEMM_SKINNY_4W_U8 = 22,
-  OCC_GEMM_SKINNY_16W_U8 = 23,
-  /* two resident workgroups per CU (independent barriers), 4 waves each */
-  OCC_GEMM_DLP_256x128x32_4W_2ST = 24,
-  OCC_GEMM_DLP_128x256x32_4W_2ST = 25,
-  OCC_GEMM_DLP_256x128x32_4W_3ST = 26,
-  OCC_GEMM_DLP_128x256x32_4W_3ST = 27,
-  /* skinny (M <= 16) with each wave's K-slice of A held in registers: B is
-     the only operand streamed per 16-column unit.  K must be a positive
-     multiple of 2048 and at most 8192 (28) / 4096 (29). */
-  OCC_GEMM_SKINNY_AREG_K8192 = 28,
-  OCC_GEMM_SKINNY_AREG_K4096 = 29,
-  /* skinny (M <= 16) with A held in registers and B staged through LDS in
-     blocks of 16 rows x 128 k (whole 256-byte row pieces per DMA
-     instruction).  K must be a positive multiple of 1024 and at most 8192;
-     automatic choice for such K when M <= 16. */
-  OCC_GEMM_SKINNY_LDSB_K8192 = 34,
-  /* B stored K x N (occ_gemm_kn / occ_gemm_kn_ex only) */
-  OCC_GEMM_KN_DLP_256x256x64_8W_2ST = 32,
-  /* skinny (M <= 16) with B stored K x N: 128-column units over the whole K,
-     4 waves splitting K, 32-row blocks of B and A streamed into LDS (2
-     stages); automatic choice for occ_gemm_kn when M <= 16. */
-  OCC_GEMM_KN_SKINNY_4W_2ST = 33
+  /* B stored K x N (occ_gemm) */
+  OCC_GEMM_KN_256x256x64_8W_2ST = 32,   /* direct-to-LDS; default for large shapes */
+  OCC_GEMM_KN_SKINNY_4W_2ST = 33,       /* M <= 16: 128-column units over the whole K; default for M <= 16 */
+  OCC_GEMM_KN_128x128x64_4W_3ST = 35,   /* default for mid-size shapes */
+  OCC_GEMM_KN_OPT1_64x64x32 = 36,       /* Table 1 opt1, one stage */
+  OCC_GEMM_KN_OPT2_64x64x64 = 37,       /* Table 1 opt2, one stage; default for small shapes */
+  OCC_GEMM_KN_128x256x32_4W_2ST = 38,   /* two resident workgroups per CU (48 KiB) */
+  /* B stored N x K (occ_gemm_bt) */
+  OCC_GEMM_OPT1_64x64x32 = 6,           /* Table 1 opt1, register-staged, one stage */
+  OCC_GEMM_OPT2_64x64x64 = 7,           /* Table 1 opt2, register-staged, one stage; default for small shapes */
+  OCC_GEMM_DL_128x128x64_4W_3ST = 14,   /* direct-to-LDS; default for mid-size shapes */
+  OCC_GEMM_DLP_256x256x64_8W_2ST = 16,  /* direct-to-LDS; default for large shapes */
+  OCC_GEMM_SKINNY_8W_U8 = 21,           /* M <= 16, any K: 8 waves, 8 k-blocks in flight per lane */
+  OCC_GEMM_DLP_128x256x32_4W_2ST = 25,  /* two resident workgroups per CU (48 KiB) */
+  OCC_GEMM_SKINNY_LDSB_K8192 = 34       /* M <= 16, K a multiple of 1024 up to 8192: A in registers,
+                                           B staged through LDS; default for such K */
 };
 
 /*
- * occ_gemm_ex -- occ_gemm with an explicit kernel variant and grid cap.
- * grid_cap > 0 launches at most grid_cap workgroups, each looping over output
- * tiles (persistent workgroups): the "thread-block count" knob of the paper's
- * Figs. 2-3.  grid_cap == 0 launches one workgroup per tile.  The grid cap
- * and the pad never change the result.  The tiled variants (1-7, 9-19, 24-27)
- * accumulate every output over k in the same order and give bit-identical
- * results; the skinny variants (8, 20-23, 28, 29, 34) split K across waves and
- * may differ from them, and from each other, in the last bit.  OCC_EINVAL for
- * an unknown variant, a skinny variant with M > 16, a K that variant 28/29/34
- * does not take, or K above 4 M for a direct-to-LDS variant with 256-row
- * tiles (8 M with 128-row tiles: variants 10-19, 24-27 and 32 address an
- * operand tile with 32-bit offsets; for such K the automatic choice falls
- * back to a register-staged variant).
+ * occ_gemm_ex -- occ_gemm with an explicit kernel variant (0 or a K x N one)
+ * and grid cap.  grid_cap > 0 launches at most grid_cap workgroups, each
+ * looping over output tiles (persistent workgroups): the "thread-block count"
+ * knob of the paper's Figs. 2-3.  grid_cap == 0 launches one workgroup per
+ * tile.  The grid cap and the pad never change the result, and the tiled
+ * variants of one layout accumulate every output over k in the same order
+ * and give bit-identical results; the skinny variants split K across waves
+ * and may differ from them in the last bit.  OCC_EINVAL for an unknown
+ * variant, a variant of the other layout, a skinny variant with M > 16, or a
+ * K or N beyond the variant's addressing limit.
  */
 int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 int variant, int grid_cap, void *stream);
 
 /*
- * occ_gemm_kn -- C = A * B with B stored K x N (row-major, N-contiguous):
- *   C[m][n] = sum_k A[m][k] * B[k][n].  Same arithmetic, rounding and LDS pad
- * as occ_gemm; the B tile is staged in LDS as stored and its MFMA operands
- * are read with gfx950's LDS transpose reads.  For M > 16 the results are
- * bit-identical to occ_gemm's default 256x256 tile on the transposed B (same
- * order of the k sums); for M <= 16 a skinny kernel (variant 33) splits K
- * across waves and may differ from it in the last bit.
- * Requirements: as occ_gemm, plus N % 8 == 0 (16-byte B rows), N at most
- * 16 M and K at most 4 M (a k-step of B and a tile of A are addressed with
- * 32-bit offsets; larger is OCC_EINVAL).
+ * occ_gemm_bt -- C = A * B^T with B stored N x K (row-major, K-contiguous:
+ * the weight layout of a linear layer, op(B) = B^T in Background, item 1):
+ *   C[m][n] = sum_k A[m][k] * B[n][k].
+ * Same arithmetic, rounding, LDS pad and errors as occ_gemm; N need not be a
+ * multiple of 8.  For M > 16 the results are bit-identical to occ_gemm on the
+ * same matrix stored K x N (same tiles, same order of the k sums); for M <= 16
+ * the skinny kernels of the two layouts split K differently and may differ in
+ * the last bit.  Any K % 8 == 0 is taken (K beyond a direct-to-LDS tile's
+ * 32-bit addressing runs on the register-staged 64x64 tile).
  */
-int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+int occ_gemm_bt(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 void *stream);
 
-/* occ_gemm_kn_ex -- occ_gemm_kn with a variant (0 = automatic,
-   OCC_GEMM_KN_DLP_256x256x64_8W_2ST, or OCC_GEMM_KN_SKINNY_4W_2ST for
-   M <= 16) and a grid cap as in occ_gemm_ex.  OCC_EINVAL for a variant that
-   reads B as N x K, or the skinny one with M > 16. */
-int occ_gemm_kn_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+/* occ_gemm_bt_ex -- occ_gemm_bt with a variant (0 or an N x K one) and a grid
+   cap as in occ_gemm_ex.  OCC_EINVAL for a K x N variant, a skinny variant
+   with M > 16, or a K that variant 34 does not take. */
+int occ_gemm_bt_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                    int variant, int grid_cap, void *stream);
 
 /* Launch plan occ_gemm_ex would use, for reporting and sweeps. */
@@ -174,29 +143,26 @@ typedef struct occ_gemm_plan {
 
 /*
  * occ_gemm_plan_query -- the plan for occ_gemm_ex(M, N, K, lds_bytes,
- * variant, grid_cap) on the current device (for a K x N variant, the plan
- * for occ_gemm_kn_ex).  Returns OCC_ELDS when
+ * variant, grid_cap) on the current device.  Returns OCC_ELDS when
  * S_tile + lds_bytes exceeds the per-workgroup LDS limit (the plan is still
- * filled in, with wg_per_cu = 0).
+ * filled in, with wg_per_cu = 0); OCC_EINVAL for an N x K variant.
  */
 int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                         occ_gemm_plan *plan);
 
-/* occ_gemm_kn_plan_query -- the plan for occ_gemm_kn_ex(M, N, K, lds_bytes,
-   variant, grid_cap): as occ_gemm_plan_query, with variant 0 standing for
-   occ_gemm_kn's automatic choice.  OCC_EINVAL for a variant that reads B as
-   N x K. */
-int occ_gemm_kn_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
+/* occ_gemm_bt_plan_query -- the same for occ_gemm_bt_ex (variant 0 standing
+   for occ_gemm_bt's automatic choice); OCC_EINVAL for a K x N variant. */
+int occ_gemm_bt_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                            occ_gemm_plan *plan);
 
 /*
- * occ_gemm_info -- the three LDS figures of Section 3.1 for the kernel used
- * on large shapes (variant 16): its tile's own LDS (S_tile), the device's
- * per-workgroup LDS limit and its LDS per CU, in bytes; so a caller can
- * size lds_bytes (S_tile + pad <= max_lds_per_wg; resident workgroups per CU
- * <= lds_per_cu / (S_tile + pad)).  occ_gemm_plan_query gives the same for
- * any shape and variant.  OCC_EINVAL for a null pointer; OCC_ENODEV without
- * a gfx950 device.
+ * occ_gemm_info -- the three LDS figures of Section 3.1 for the kernel
+ * occ_gemm uses on large shapes (variant 32): its tile's own LDS (S_tile),
+ * the device's per-workgroup LDS limit and its LDS per CU, in bytes; so a
+ * caller can size lds_bytes (S_tile + pad <= max_lds_per_wg; resident
+ * workgroups per CU <= lds_per_cu / (S_tile + pad)).  occ_gemm_plan_query
+ * gives the same for any shape and variant.  OCC_EINVAL for a null pointer;
+ * OCC_ENODEV without a gfx950 device.
  */
 int occ_gemm_info(int *tile_lds_bytes, int *max_lds_per_wg, int *lds_per_cu);
 
@@ -282,16 +248,47 @@ enum { OCC_RUN_SEQ = 1, OCC_RUN_OVL = 2, OCC_RUN_ISO = 4, OCC_RUN_GRAPH = 8, OCC
    GPU's memory (the multi-GPU setting of Section 4): the local kernel then
    streams at the link rate in the sequential schedule too. */
 
+/* Layout of B in the schedule's GEMM (occ_overlap_cfg.gemm_b_layout). */
+enum { OCC_B_KN = 0 /* K x N, occ_gemm */, OCC_B_NK = 1 /* N x K, occ_gemm_bt */ };
+
+/*
+ * The per-iteration dependency K_g^i -> K_c^i of the overlapped schedule
+ * (occ_overlap_cfg.dep; Section 3.2):
+ *   OCC_DEP_EVENT   -- a runtime event recorded on the compute stream after
+ *                      K_g^i and waited on by the comm stream before K_c^i
+ *                      (the paper's form).  Costs about 18 us of host issue
+ *                      time per iteration on MI355X, so schedules whose
+ *                      kernels are that short become bound by it.
+ *   OCC_DEP_COUNTER -- a device-side counter: every workgroup of K_g^i adds
+ *                      one to a per-iteration counter when it is done (after
+ *                      its stores, released at device scope), and every
+ *                      workgroup of K_c^i waits until the counter reaches
+ *                      K_g^i's workgroup count (then acquires) before it
+ *                      reads anything.  No host call besides the two kernel
+ *                      launches.  The collective's last workgroup puts the
+ *                      counter back to zero.  The wait is bounded: a
+ *                      workgroup that has waited 2 s skips its work and the
+ *                      schedule fails with OCC_ETIMEOUT.  Needs a GEMM and a
+ *                      collective that fit on one CU side by side (one comm
+ *                      workgroup per CU at most, registers and LDS of both
+ *                      within the CU's), else OCC_EINVAL; n_iter <= 1024;
+ *                      not with OCC_RUN_GRAPH (a replayed graph may order
+ *                      a collective before its GEMM on one queue, and that
+ *                      collective would wait out its bound): OCC_EINVAL.
+ * The sequential schedule needs no dependency (one stream).
+ */
+enum { OCC_DEP_EVENT = 0, OCC_DEP_COUNTER = 1 };
+
 typedef struct occ_overlap_cfg {
-  /* K_g: as occ_gemm */
+  /* K_g: as occ_gemm (gemm_b_layout OCC_B_KN) or occ_gemm_bt (OCC_B_NK) */
   int M, N, K;
   const void *A, *B;
   void *C;
   size_t lds_bytes;         /* extra LDS per GEMM workgroup (Section 3.1) */
-  int gemm_variant;         /* OCC_GEMM_* (0 = automatic) */
+  int gemm_variant;         /* OCC_GEMM_* of the layout (0 = automatic) */
   int gemm_grid;            /* 0: one workgroup per tile; > 0: persistent grid cap */
   int gemm_priority;        /* wave priority of the GEMM kernel, 0 (normal) .. 3 */
-  /* (gemm_b_layout is at the end of the structure) */
+  int gemm_b_layout;        /* OCC_B_KN (default) or OCC_B_NK */
   /* K_c: as share_reduce (comm_kind 0), share_permute (comm_kind 1) or
      share_reduce_own of the GEMM's output (comm_kind 2, bufs/nchunks = the
      fp32 peer chunks) */
@@ -306,11 +303,25 @@ typedef struct occ_overlap_cfg {
   size_t chunk_bytes;
   int comm_wgs;             /* workgroups of the comm kernel; 0 = library default */
   int comm_priority;        /* wave priority of the comm kernel, 0 (normal) .. 3 (highest) */
+  /* bandwidth pacing of the collective in the overlapped schedule, GB/s over
+     the whole grid: every comm wave spaces its load/store trips so that the
+     kernel streams at no more than this rate, leaving memory bandwidth to the
+     co-running GEMM.  0 = unpaced (full speed); otherwise at least
+     OCC_MIN_COMM_RATE_GBS.  The sequential schedule and the isolated kernel
+     timings run unpaced, so t_seq stays the fastest sequential makespan,
+     unless flags has OCC_RUN_PACE_ALL.  Results are unchanged (same
+     arithmetic, same order). */
+  double comm_rate_gbs;
   /* schedule (Section 3.2) and protocol (Section 4.1) */
   int n_iter;               /* GEMM -> collective iterations per schedule, >= 1 */
+  int dep;                  /* OCC_DEP_EVENT (default) or OCC_DEP_COUNTER */
   int reps;                 /* timed repetitions of each pass, >= 1 */
   int warmup;               /* untimed repetitions before them, >= 0 */
   int flags;                /* OCC_RUN_* bits, 0 = all */
+  /* the caller's stream (hipStream_t as void*, NULL = the null stream): the
+     launcher's work starts after everything already enqueued on it, so
+     inputs the caller is still producing there are complete first */
+  void *stream;
   /* optional device buffer of 4*n_iter uint64: for the last overlapped
      repetition, [start_G0, end_G0, start_C0, end_C0, start_G1, ...] in
      10 ns ticks of the GPU's constant-rate clock (earliest workgroup start,
@@ -327,24 +338,13 @@ typedef struct occ_overlap_cfg {
      Records beyond wg_trace_cap are counted but not written.  NULL = off. */
   uint32_t *wg_trace;
   int wg_trace_cap;
-  /* bandwidth pacing of the collective in the overlapped schedule, GB/s over
-     the whole grid: every comm wave spaces its load/store trips so that the
-     kernel streams at no more than this rate, leaving memory bandwidth to the
-     co-running GEMM.  0 = unpaced (full speed); otherwise at least
-     OCC_MIN_COMM_RATE_GBS.  The sequential schedule and the isolated kernel
-     timings run unpaced, so t_seq stays the fastest sequential makespan,
-     unless flags has OCC_RUN_PACE_ALL.  Results are unchanged (same
-     arithmetic, same order). */
-  double comm_rate_gbs;
-  /* layout of B: 0 = N x K (occ_gemm), 1 = K x N (occ_gemm_kn) */
-  int gemm_b_layout;
 } occ_overlap_cfg;
 
 #define OCC_MIN_COMM_RATE_GBS 10.0
 
 typedef struct occ_overlap_result {
   double t_seq_ms;        /* mean sequential makespan: one stream, G0 C0 G1 C1 ... */
-  double t_ovl_ms;        /* mean overlapped makespan: two streams + per-iteration event */
+  double t_ovl_ms;        /* mean overlapped makespan: two streams + per-iteration dependency */
   double t_seq_min_ms, t_ovl_min_ms;
   double reduction_pct;   /* 100 * (1 - t_ovl / t_seq) = 100 * (1 - TimeRatio) */
   double t_gemm_ms;       /* mean duration of one GEMM launch, isolated pass */
@@ -364,8 +364,11 @@ typedef struct occ_overlap_result {
  * Both schedules end on the compute stream: the overlapped one forks the comm
  * stream off it with an event and joins it back after the last collective.
  * Host-synchronous.  Uses two library-owned streams of default priority on
- * the current device (created once, kept for the process); the collective's
- * precedence (Section 3.3) is the comm kernel's wave priority.  All three
+ * the current device (created once, kept for the process), which first wait
+ * for the work already enqueued on cfg->stream; the collective's
+ * precedence (Section 3.3) is the comm kernel's wave priority.  With
+ * OCC_DEP_COUNTER the per-iteration counters live in a small device buffer
+ * the library allocates once per device (8 KiB).  All three
  * passes compute the same outputs: C, out/dst are identical to one occ_gemm
  * and one share_* call.  Buffers are validated as by those entry points.
  * HIP maps a process's streams onto a fixed number of hardware queues
@@ -383,15 +386,18 @@ int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
  * runtime policy the paper leaves to future work (Section 6).  Times the
  * overlapped schedule of *cfg (tune_reps repetitions after one warm-up) for
  * every candidate in
- *   comm_priority {0, 3} x comm_wgs {library default (one per CU), two per CU}
+ *   comm_priority {0, 3} x comm_wgs {library default (one per CU), two per CU,
+ *                                     one per four CUs}
  *   x gemm_grid {one workgroup per tile, one persistent workgroup per CU}
  *   x lds_bytes {0, the pad that lowers the GEMM's residency by one
- *                workgroup per CU (only when it has more than one)},
- * writes the fastest setting into those fields of *cfg (gemm_variant,
- * n_iter, buffers and the rest are kept), then runs run_overlap(cfg, res)
- * with it.  *prefer_sequential is set to 1 when even the best overlapped
- * makespan is longer than the sequential one (then overlap should be off).
- * Same validation and errors as run_overlap; host-synchronous.
+ *                workgroup per CU (only when it has more than one)}
+ *   x dep {OCC_DEP_EVENT, OCC_DEP_COUNTER (with one comm workgroup per CU)},
+ * writes the setting with the shortest median makespan into those fields of
+ * *cfg (gemm_variant, n_iter, buffers and the rest are kept), then runs
+ * run_overlap(cfg, res) with it.  *prefer_sequential is set to 1 when even
+ * the best overlapped median makespan is longer than the sequential one
+ * (then overlap should be off).  Same validation and errors as run_overlap;
+ * host-synchronous.
  */
 int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                      int *prefer_sequential);
@@ -402,8 +408,8 @@ const char *occ_strerror(int status);
 /* Library version, (major << 16) | minor.  The minor number grows whenever a
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
-#define OCC_VERSION_MAJOR 1
-#define OCC_VERSION_MINOR 4
+#define OCC_VERSION_MAJOR 2
+#define OCC_VERSION_MINOR 0
 int occ_version(void);
 
 #ifdef __cplusplus

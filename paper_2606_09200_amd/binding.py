@@ -17,26 +17,24 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libocc.so")
 
-OCC_OK, OCC_EINVAL, OCC_ELDS, OCC_EPERM, OCC_EALIAS, OCC_EHIP, OCC_ENODEV = 0, -1, -2, -3, -4, -5, -6
+OCC_OK, OCC_EINVAL, OCC_ELDS, OCC_EPERM, OCC_EALIAS, OCC_EHIP, OCC_ENODEV, OCC_ETIMEOUT = 0, -1, -2, -3, -4, -5, -6, -7
 OCC_COMM_REDUCE, OCC_COMM_PERMUTE, OCC_COMM_REDUCE_OWN = 0, 1, 2
 OCC_RUN_SEQ, OCC_RUN_OVL, OCC_RUN_ISO, OCC_RUN_GRAPH, OCC_RUN_PACE_ALL = 1, 2, 4, 8, 16
-GEMM_VARIANTS = {
-    0: "auto", 1: "256x256x64 4w", 2: "256x256x64 8w", 3: "256x128x64 4w",
-    4: "256x128x64 4w 1-stage", 5: "128x128x64 4w", 6: "opt1 64x64x32", 7: "opt2 64x64x64",
-    8: "skinny M<=16", 9: "256x256x32 4w 1-stage",
-    10: "dl 256x256x64 8w 2st", 11: "dl 256x256x32 8w 4st", 12: "dl 256x256x32 8w 3st",
-    13: "dl 256x128x64 4w 3st", 14: "dl 128x128x64 4w 3st", 15: "dl 256x128x64 8w 3st",
-    16: "dl+pipe 256x256x64 8w 2st", 17: "dl+pipe 256x256x32 8w 4st",
-    18: "dl+pipe 256x128x64 4w 3st", 19: "dl+pipe 256x256x64 4w 2st",
-    20: "skinny 8w u16", 21: "skinny 8w u8", 22: "skinny 4w u8", 23: "skinny 16w u8",
-    24: "dl+pipe 256x128x32 4w 2st 2wg/cu", 25: "dl+pipe 128x256x32 4w 2st 2wg/cu",
-    26: "dl+pipe 256x128x32 4w 3st 2wg/cu", 27: "dl+pipe 128x256x32 4w 3st 2wg/cu",
-    28: "skinny A-in-registers K<=8192", 29: "skinny A-in-registers K<=4096",
-    32: "dl+pipe 256x256x64 8w 2st, B K x N",
+OCC_B_KN, OCC_B_NK = 0, 1
+OCC_DEP_EVENT, OCC_DEP_COUNTER = 0, 1
+# kernel variants of occ.h, by the layout of B they read
+KN_VARIANTS = {
+    32: "dl+pipe 256x256x64 8w 2st", 33: "skinny M<=16, 128-column units",
+    35: "dl 128x128x64 4w 3st", 36: "opt1 64x64x32 1st", 37: "opt2 64x64x64 1st",
+    38: "dl+pipe 128x256x32 4w 2st 2wg/cu",
 }
-KN_VARIANTS = (32, 33)    # take B stored K x N (occ_gemm_kn_ex only); 33: M <= 16
-SKINNY_VARIANTS = (8, 20, 21, 22, 23, 28, 29)
-ABI_VERSION = (1, 4)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+NK_VARIANTS = {
+    6: "opt1 64x64x32 register-staged", 7: "opt2 64x64x64 register-staged",
+    14: "dl 128x128x64 4w 3st", 16: "dl+pipe 256x256x64 8w 2st", 21: "skinny M<=16, 8w, 8 k-blocks in flight",
+    25: "dl+pipe 128x256x32 4w 2st 2wg/cu", 34: "skinny M<=16, A in registers, B through LDS (K%1024==0, K<=8192)",
+}
+SKINNY_VARIANTS = (21, 33, 34)     # M <= 16 only
+ABI_VERSION = (2, 0)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -58,15 +56,15 @@ class occ_overlap_cfg(ctypes.Structure):
         ("M", ctypes.c_int), ("N", ctypes.c_int), ("K", ctypes.c_int),
         ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
         ("lds_bytes", ctypes.c_size_t), ("gemm_variant", ctypes.c_int), ("gemm_grid", ctypes.c_int),
-        ("gemm_priority", ctypes.c_int),
+        ("gemm_priority", ctypes.c_int), ("gemm_b_layout", ctypes.c_int),
         ("comm_kind", ctypes.c_int), ("bufs", ctypes.POINTER(ctypes.c_void_p)),
         ("nchunks", ctypes.c_int), ("len", ctypes.c_size_t), ("out", ctypes.c_void_p),
         ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("perm", ctypes.POINTER(ctypes.c_int32)),
         ("chunk_bytes", ctypes.c_size_t), ("comm_wgs", ctypes.c_int), ("comm_priority", ctypes.c_int),
-        ("n_iter", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
-        ("flags", ctypes.c_int), ("timeline", ctypes.c_void_p),
+        ("comm_rate_gbs", ctypes.c_double),
+        ("n_iter", ctypes.c_int), ("dep", ctypes.c_int), ("reps", ctypes.c_int), ("warmup", ctypes.c_int),
+        ("flags", ctypes.c_int), ("stream", ctypes.c_void_p), ("timeline", ctypes.c_void_p),
         ("wg_trace", ctypes.c_void_p), ("wg_trace_cap", ctypes.c_int),
-        ("comm_rate_gbs", ctypes.c_double), ("gemm_b_layout", ctypes.c_int),
     ]
 
 
@@ -84,12 +82,12 @@ _SIGS = {
     "occ_gemm": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
     "occ_gemm_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
                     ctypes.c_int, ctypes.c_int, _P],
-    "occ_gemm_kn": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
-    "occ_gemm_kn_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
+    "occ_gemm_bt": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, _P],
+    "occ_gemm_bt_ex": [_P, _P, _P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t,
                        ctypes.c_int, ctypes.c_int, _P],
     "occ_gemm_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                             ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
-    "occ_gemm_kn_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
+    "occ_gemm_bt_plan_query": [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_size_t, ctypes.c_int,
                                ctypes.c_int, ctypes.POINTER(occ_gemm_plan)],
     "occ_gemm_info": [ctypes.POINTER(ctypes.c_int)] * 3,
     "share_reduce": [ctypes.POINTER(_P), ctypes.c_int, ctypes.c_size_t, _P, _P],
@@ -152,7 +150,7 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
 
 
-def _gemm_args(A, B, C, b_kn=False):
+def _gemm_args(A, B, C, b_kn=True):
     for name, t in (("A", A), ("B", B), ("C", C)):
         if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous() or t.dim() != 2:
             raise ValueError("%s must be a contiguous 2-D bfloat16 GPU tensor" % name)
@@ -164,7 +162,7 @@ def _gemm_args(A, B, C, b_kn=False):
 
 
 def occ_gemm(A, B, C, lds_bytes=0, stream=None):
-    """C = A @ B.T (bf16, fp32 accumulation); B is N x K."""
+    """C = A @ B (bf16, fp32 accumulation); B is K x N."""
     M, N, K = _gemm_args(A, B, C)
     _check(lib().occ_gemm(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), _stream(stream)),
            "occ_gemm")
@@ -172,33 +170,35 @@ def occ_gemm(A, B, C, lds_bytes=0, stream=None):
 
 
 def occ_gemm_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
+    """occ_gemm with a K x N kernel variant and a persistent grid cap."""
     M, N, K = _gemm_args(A, B, C)
     _check(lib().occ_gemm_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
                              int(grid_cap), _stream(stream)), "occ_gemm_ex")
     return C
 
 
-def occ_gemm_kn(A, B, C, lds_bytes=0, stream=None):
-    """C = A @ B (bf16, fp32 accumulation); B is K x N."""
-    M, N, K = _gemm_args(A, B, C, b_kn=True)
-    _check(lib().occ_gemm_kn(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), _stream(stream)),
-           "occ_gemm_kn")
+def occ_gemm_bt(A, B, C, lds_bytes=0, stream=None):
+    """C = A @ B.T (bf16, fp32 accumulation); B is N x K (a linear layer's weight)."""
+    M, N, K = _gemm_args(A, B, C, b_kn=False)
+    _check(lib().occ_gemm_bt(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), _stream(stream)),
+           "occ_gemm_bt")
     return C
 
 
-def occ_gemm_kn_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
-    M, N, K = _gemm_args(A, B, C, b_kn=True)
-    _check(lib().occ_gemm_kn_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
-                                int(grid_cap), _stream(stream)), "occ_gemm_kn_ex")
+def occ_gemm_bt_ex(A, B, C, lds_bytes=0, variant=0, grid_cap=0, stream=None):
+    """occ_gemm_bt with an N x K kernel variant and a persistent grid cap."""
+    M, N, K = _gemm_args(A, B, C, b_kn=False)
+    _check(lib().occ_gemm_bt_ex(_ptr(A), _ptr(B), _ptr(C), M, N, K, int(lds_bytes), int(variant),
+                                int(grid_cap), _stream(stream)), "occ_gemm_bt_ex")
     return C
 
 
-def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False, b_layout="nk"):
+def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False, b_layout="kn"):
     """Plan as a dict; 'feasible' is False when the pad does not fit (OCC_ELDS).
-    b_layout "kn" asks for occ_gemm_kn's plan (occ_gemm_kn_plan_query)."""
+    b_layout "kn" (default) is occ_gemm's plan, "nk" occ_gemm_bt's."""
     if b_layout not in ("nk", "kn"):
-        raise ValueError("b_layout must be 'nk' or 'kn'")
-    name = "occ_gemm_kn_plan_query" if b_layout == "kn" else "occ_gemm_plan_query"
+        raise ValueError("b_layout must be 'kn' or 'nk'")
+    name = "occ_gemm_plan_query" if b_layout == "kn" else "occ_gemm_bt_plan_query"
     p = occ_gemm_plan()
     st = getattr(lib(), name)(int(M), int(N), int(K), int(lds_bytes), int(variant), int(grid_cap),
                               ctypes.byref(p))
@@ -207,6 +207,11 @@ def occ_gemm_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=Fals
     d = {f: getattr(p, f) for f, _ in occ_gemm_plan._fields_}
     d["feasible"] = st == OCC_OK
     return d
+
+
+def occ_gemm_bt_plan_query(M, N, K, lds_bytes=0, variant=0, grid_cap=0, strict=False):
+    """occ_gemm_bt's plan (B stored N x K) as a dict, as occ_gemm_plan_query."""
+    return occ_gemm_plan_query(M, N, K, lds_bytes, variant, grid_cap, strict, b_layout="nk")
 
 
 def occ_gemm_info():
@@ -308,9 +313,11 @@ def decode_wg_trace(wg_trace):
 
 def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant, gemm_grid,
               gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup, flags, timeline, wg_trace,
-              comm_rate_gbs=0.0, b_layout="nk", reduce_own=False):
+              comm_rate_gbs=0.0, b_layout="kn", reduce_own=False, dep="event", stream=None):
     if b_layout not in ("nk", "kn"):
-        raise ValueError("b_layout must be 'nk' or 'kn'")
+        raise ValueError("b_layout must be 'kn' or 'nk'")
+    if dep not in ("event", "counter"):
+        raise ValueError("dep must be 'event' or 'counter'")
     if reduce_own:
         # C holds one M x N output per iteration; the collective reduces its own
         if C.dim() != 3 or C.shape[0] != n_iter:
@@ -324,7 +331,9 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
     cfg.lds_bytes, cfg.gemm_variant, cfg.gemm_grid = int(lds_bytes), int(gemm_variant), int(gemm_grid)
     cfg.gemm_priority = int(gemm_priority)
     cfg.comm_rate_gbs = float(comm_rate_gbs)
-    cfg.gemm_b_layout = 1 if b_layout == "kn" else 0
+    cfg.gemm_b_layout = OCC_B_KN if b_layout == "kn" else OCC_B_NK
+    cfg.dep = OCC_DEP_COUNTER if dep == "counter" else OCC_DEP_EVENT
+    cfg.stream = _stream(stream).value
     keep = []
     if reduce_own:
         arr, n = _peer_ptrs(bufs, M * N)
@@ -369,7 +378,8 @@ def _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_v
 def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
                 lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0, comm_wgs=0,
                 comm_priority=3, n_iter=10, reps=20, warmup=10, flags=0, timeline=None,
-                wg_trace=None, comm_rate_gbs=0.0, b_layout="nk", reduce_own=False):
+                wg_trace=None, comm_rate_gbs=0.0, b_layout="kn", reduce_own=False, dep="event",
+                stream=None):
     """Sequential vs overlapped makespan of n_iter GEMM -> collective iterations.
 
     Pass ``bufs``/``out`` for the allreduce share, or ``src``/``dst``/``perm``/
@@ -377,31 +387,35 @@ def run_overlap(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, 
     tensor of 4*n_iter entries (see occ_overlap_cfg.timeline).  ``wg_trace``:
     optional int32 GPU tensor of 4 + 12*cap entries (see occ_overlap_cfg.wg_trace).
     ``comm_rate_gbs``: bandwidth pacing of the collective in the overlapped
-    schedule (0 = full speed).  ``b_layout``: "nk" (B is N x K, C = A B^T) or
-    "kn" (B is K x N, C = A B).  ``reduce_own``: the collective consumes the
-    GEMM's output (OCC_COMM_REDUCE_OWN): C is (n_iter, M, N), iteration i's
-    GEMM writes C[i] and its collective is share_reduce_own(C[i], bufs, out)
-    with ``bufs`` the fp32 peer chunks (possibly none).  Returns the
-    occ_overlap_result fields as a dict.
+    schedule (0 = full speed).  ``b_layout``: "kn" (B is K x N, C = A B, the
+    default) or "nk" (B is N x K, C = A B^T).  ``reduce_own``: the collective
+    consumes the GEMM's output (OCC_COMM_REDUCE_OWN): C is (n_iter, M, N),
+    iteration i's GEMM writes C[i] and its collective is
+    share_reduce_own(C[i], bufs, out) with ``bufs`` the fp32 peer chunks
+    (possibly none).  ``dep``: the per-iteration dependency, "event" or
+    "counter" (OCC_DEP_COUNTER).  The library's streams start after the work
+    already queued on ``stream`` (default: torch's current stream).  Returns
+    the occ_overlap_result fields as a dict.
     """
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
                           gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, reps, warmup,
-                          flags, timeline, wg_trace, comm_rate_gbs, b_layout, reduce_own)
+                          flags, timeline, wg_trace, comm_rate_gbs, b_layout, reduce_own, dep, stream)
     res = occ_overlap_result()
     _check(lib().run_overlap(ctypes.byref(cfg), ctypes.byref(res)), "run_overlap")
     return {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}
 
 
 def occ_overlap_tune(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=None, chunk_bytes=0,
-                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3, b_layout="nk",
-                     reduce_own=False):
+                     gemm_variant=0, n_iter=10, reps=20, warmup=10, tune_reps=3, b_layout="kn",
+                     reduce_own=False, stream=None):
     """Adaptive knob choice (see occ.h).  Returns (chosen knobs, result dict, prefer_sequential)."""
     cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, 0, gemm_variant, 0, 0, 0,
-                          0, n_iter, reps, warmup, 0, None, None, 0.0, b_layout, reduce_own)
+                          0, n_iter, reps, warmup, 0, None, None, 0.0, b_layout, reduce_own, "event", stream)
     res = occ_overlap_result()
     pref = ctypes.c_int(0)
     _check(lib().occ_overlap_tune(ctypes.byref(cfg), int(tune_reps), ctypes.byref(res),
                                   ctypes.byref(pref)), "occ_overlap_tune")
     knobs = {"comm_priority": cfg.comm_priority, "comm_wgs": cfg.comm_wgs,
-             "gemm_grid": cfg.gemm_grid, "lds_bytes": cfg.lds_bytes}
+             "gemm_grid": cfg.gemm_grid, "lds_bytes": cfg.lds_bytes,
+             "dep": "counter" if cfg.dep == OCC_DEP_COUNTER else "event"}
     return knobs, {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}, bool(pref.value)

@@ -107,58 +107,59 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
 
 extern "C" {
 
-int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
-                int variant, int grid_cap, void *stream) {
-  int st = occ::validate_gemm(A, B, C, M, N, K);
+static int gemm_entry(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                      int variant, int grid_cap, void *stream, bool b_kn) {
+  int st = occ::validate_gemm(A, B, C, M, N, K, b_kn);
   if (st != OCC_OK) return st;
   if (grid_cap < 0 || variant < 0) return OCC_EINVAL;
-  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}};
+  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KHooks{}, b_kn};
   return occ::gemm_launch(c, static_cast<hipStream_t>(stream));
+}
+
+static int plan_entry(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap, occ_gemm_plan *plan,
+                      bool b_kn) {
+  if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
+  memset(plan, 0, sizeof *plan);
+  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KHooks{}, b_kn};
+  return occ::gemm_plan(c, plan);
+}
+
+int occ_gemm_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+                int variant, int grid_cap, void *stream) {
+  return gemm_entry(A, B, C, M, N, K, lds_bytes, variant, grid_cap, stream, true);
 }
 
 int occ_gemm(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
              void *stream) {
-  return occ_gemm_ex(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream);
+  return gemm_entry(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream, true);
 }
 
-int occ_gemm_kn_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+int occ_gemm_bt_ex(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                    int variant, int grid_cap, void *stream) {
-  int st = occ::validate_gemm(A, B, C, M, N, K, true);
-  if (st != OCC_OK) return st;
-  if (grid_cap < 0 || variant < 0) return OCC_EINVAL;
-  occ::GemmCall c{A, B, C, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0}, true};
-  return occ::gemm_launch(c, static_cast<hipStream_t>(stream));
+  return gemm_entry(A, B, C, M, N, K, lds_bytes, variant, grid_cap, stream, false);
 }
 
-int occ_gemm_kn(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
+int occ_gemm_bt(const void *A, const void *B, void *C, int M, int N, int K, size_t lds_bytes,
                 void *stream) {
-  return occ_gemm_kn_ex(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream);
+  return gemm_entry(A, B, C, M, N, K, lds_bytes, OCC_GEMM_AUTO, 0, stream, false);
 }
 
 int occ_gemm_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                         occ_gemm_plan *plan) {
-  if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
-  memset(plan, 0, sizeof *plan);
-  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0},
-                  occ::gemm_variant_is_kn(variant)};
-  return occ::gemm_plan(c, plan);
+  return plan_entry(M, N, K, lds_bytes, variant, grid_cap, plan, true);
 }
 
-int occ_gemm_kn_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
+int occ_gemm_bt_plan_query(int M, int N, int K, size_t lds_bytes, int variant, int grid_cap,
                            occ_gemm_plan *plan) {
-  if (plan == nullptr || M < 0 || N < 0 || K < 0 || variant < 0 || grid_cap < 0) return OCC_EINVAL;
-  memset(plan, 0, sizeof *plan);
-  occ::GemmCall c{nullptr, nullptr, nullptr, M, N, K, lds_bytes, grid_cap, variant, 0, occ::KTrace{nullptr, nullptr, 0, 0},
-                  true};
-  return occ::gemm_plan(c, plan);
+  return plan_entry(M, N, K, lds_bytes, variant, grid_cap, plan, false);
 }
 
 int occ_gemm_info(int *tile_lds_bytes, int *max_lds_per_wg, int *lds_per_cu) {
   if (tile_lds_bytes == nullptr || max_lds_per_wg == nullptr || lds_per_cu == nullptr) return OCC_EINVAL;
   occ_gemm_plan p;
-  // the kernel the library picks for large shapes (any shape with at least
-  // one 256x256 tile per CU takes it)
-  int st = occ_gemm_plan_query(8192, 8192, 8192, 0, OCC_GEMM_DLP_256x256x64_8W_2ST, 0, &p);
+  // the kernel occ_gemm picks for large shapes (any shape with at least one
+  // 256x256 tile per CU takes it)
+  int st = occ_gemm_plan_query(8192, 8192, 8192, 0, OCC_GEMM_KN_256x256x64_8W_2ST, 0, &p);
   if (st != OCC_OK) return st;
   *tile_lds_bytes = p.tile_lds_bytes;
   *max_lds_per_wg = p.max_lds_per_wg;
@@ -173,7 +174,7 @@ int share_reduce_ex(const float *const *bufs, int nchunks, size_t len, float *ou
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (len > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0};
+  occ::ReduceCall c{bufs, nchunks, len, out, wgs, priority, occ::KHooks{}, 0.0};
   return occ::reduce_launch(c, static_cast<hipStream_t>(stream));
 }
 
@@ -188,7 +189,7 @@ int share_reduce_own(const void *own, const float *const *peers, int npeers, siz
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (len > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::ReduceCall c{peers, npeers, len, out, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0,
+  occ::ReduceCall c{peers, npeers, len, out, wgs, priority, occ::KHooks{}, 0.0,
                     static_cast<const uint16_t *>(own)};
   return occ::reduce_launch(c, static_cast<hipStream_t>(stream));
 }
@@ -200,7 +201,7 @@ int share_permute_ex(const void *src, void *dst, const int32_t *perm, int nchunk
   if (wgs < 0 || priority < 0 || priority > 3) return OCC_EINVAL;
   const occ::DeviceInfo *di = nullptr;
   if (chunk_bytes > 0 && (st = occ::current_device_info(&di)) != OCC_OK) return st;
-  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, occ::KTrace{nullptr, nullptr, 0, 0}, 0.0};
+  occ::PermuteCall c{src, dst, perm, nchunks, chunk_bytes, wgs, priority, occ::KHooks{}, 0.0};
   return occ::permute_launch(c, static_cast<hipStream_t>(stream));
 }
 
@@ -227,6 +228,7 @@ const char *occ_strerror(int status) {
     case OCC_EALIAS: return "OCC_EALIAS: an output overlaps an input";
     case OCC_EHIP: return "OCC_EHIP: HIP runtime error";
     case OCC_ENODEV: return "OCC_ENODEV: no gfx950 device is current";
+    case OCC_ETIMEOUT: return "OCC_ETIMEOUT: a collective's bounded wait for its GEMM ran out";
     default: return "unknown occ status";
   }
 }

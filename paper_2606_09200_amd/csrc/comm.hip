@@ -60,14 +60,14 @@ template <int NC, int UNROLL, bool OFF32, bool OWN>
 __global__ __launch_bounds__(kReduceThreads) void reduce_vec_kernel(ChunkPtrs cp, int nchunks, size_t nvec,
                                                                     float *__restrict__ out,
                                                                     const uint16_t *__restrict__ own, int prio,
-                                                                    uint32_t pace, KTrace tr) {
+                                                                    uint32_t pace, KHooks tr) {
   // OFF32: every byte offset the loop forms fits in 32 bits (checked by the
   // host), so each access is a scalar base plus one shared 32-bit lane
   // offset instead of a 64-bit address per chunk: fewer vector instructions
   // per byte, which is issue time a co-running GEMM on the same SIMD gets back.
   using I = typename std::conditional<OFF32, uint32_t, size_t>::type;
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   Pacer pc = pace_start(pace);
   const int nc = NC > 0 ? NC : nchunks;
   const I n = (I)nvec;
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_vec_kernel(ChunkPtrs cp
     }
     st(acc, i);
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 // Scalar path: elements [first, len) one at a time (the tail after the vector
@@ -148,16 +148,16 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_scalar_kernel(ChunkPtrs
                                                                        size_t first, size_t len,
                                                                        float *__restrict__ out,
                                                                        const uint16_t *__restrict__ own,
-                                                                       int prio, KTrace tr) {
+                                                                       int prio, KHooks tr) {
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   const size_t stride = (size_t)gridDim.x * kReduceThreads;
   for (size_t j = first + (size_t)blockIdx.x * kReduceThreads + threadIdx.x; j < len; j += stride) {
     float acc = own != nullptr ? widen_bf16(own[j]) : cp.p[0][j];
     for (int c = own != nullptr ? 0 : 1; c < nchunks; ++c) acc = acc + cp.p[c][j];
     out[j] = acc;
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 struct PermTable {
@@ -171,12 +171,12 @@ template <int UNROLL, bool OFF32>
 __global__ __launch_bounds__(kPermuteThreads) void permute_vec_kernel(const u32x4 *__restrict__ src,
                                                                       u32x4 *__restrict__ dst, PermTable pt,
                                                                       int nchunks, size_t cvec, int parts,
-                                                                      int prio, uint32_t pace, KTrace tr) {
+                                                                      int prio, uint32_t pace, KHooks tr) {
   // OFF32: offsets inside a chunk fit in 32 bits (checked by the host): the
   // work item's chunk bases are scalar and the lanes share one 32-bit offset.
   using I = typename std::conditional<OFF32, uint32_t, size_t>::type;
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   Pacer pc = pace_start(pace);
   bool first = true;
   const int nwork = nchunks * parts;
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kPermuteThreads) void permute_vec_kernel(const u32x
     }
     for (; i < hi; i += kPermuteThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(at(s, i)), atw(d, i));
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 // Byte path for unaligned buffers or chunk sizes.
@@ -209,16 +209,16 @@ __global__ __launch_bounds__(kPermuteThreads) void permute_byte_kernel(const uin
                                                                        uint8_t *__restrict__ dst,
                                                                        PermTable pt, int nchunks,
                                                                        size_t chunk_bytes, int prio,
-                                                                       KTrace tr) {
+                                                                       KHooks tr) {
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   const size_t stride = (size_t)gridDim.x * kPermuteThreads;
   for (int c = 0; c < nchunks; ++c) {
     const uint8_t *s = src + (size_t)pt.p[c] * chunk_bytes;
     uint8_t *d = dst + (size_t)c * chunk_bytes;
     for (size_t b = (size_t)blockIdx.x * kPermuteThreads + threadIdx.x; b < chunk_bytes; b += stride) d[b] = s[b];
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 __global__ void stamps_reset_kernel(uint64_t *stamps, int npairs, uint32_t *wg) {
@@ -264,7 +264,7 @@ uint32_t pace_ticks(double trip_bytes, double rate_gbs) {
 
 template <bool OFF32, bool OWN>
 void launch_reduce(int nchunks, int g, hipStream_t s, const ChunkPtrs &cp, size_t nvec, float *out,
-                   const uint16_t *own, int prio, uint32_t pace, const KTrace &tr) {
+                   const uint16_t *own, int prio, uint32_t pace, const KHooks &tr) {
   // instantiations by the number of terms (own + fp32 chunks)
   switch (nchunks + (OWN ? 1 : 0)) {
     case 2: hipLaunchKernelGGL((reduce_vec_kernel<OWN ? 1 : 2, reduce_unroll(2), OFF32, OWN>), dim3(g), dim3(kReduceThreads), 0, s, cp, nchunks, nvec, out, own, prio, pace, tr); break;
@@ -293,8 +293,13 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
   }
   int wgs = c.wgs > 0 ? c.wgs : reduce_default_wgs(c);
   const int prio = c.priority;
+  // a dependency wait is acknowledged by every workgroup of every kernel below
+  KHooks tr = c.trace;
   if (vec) {
     size_t nvec = c.len / 4;
+    const bool tail = nvec * 4 < c.len;
+    if (tr.wait != nullptr)
+      tr.ack_target = (nvec > 0 ? (uint32_t)clamp_wgs(nvec, wgs, kReduceThreads) : 0u) + (tail ? 1u : 0u);
     if (nvec > 0) {
       int g = clamp_wgs(nvec, wgs, kReduceThreads);
       // positions per lane per trip of each instantiation, and the bytes
@@ -307,20 +312,21 @@ int reduce_launch(const ReduceCall &c, hipStream_t s) {
       // plus one unrolled grid stride) * 16, stays below 2^32
       const bool off32 = ((double)nvec + 4.0 * g * kReduceThreads) * 16.0 < 4294967296.0;
       if (own) {
-        if (off32) launch_reduce<true, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
-        else launch_reduce<false, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, c.trace);
+        if (off32) launch_reduce<true, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, tr);
+        else launch_reduce<false, true>(c.nchunks, g, s, cp, nvec, c.out, c.own, prio, pace, tr);
       } else {
-        if (off32) launch_reduce<true, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, c.trace);
-        else launch_reduce<false, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, c.trace);
+        if (off32) launch_reduce<true, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, tr);
+        else launch_reduce<false, false>(c.nchunks, g, s, cp, nvec, c.out, nullptr, prio, pace, tr);
       }
     }
-    size_t first = nvec * 4;
-    if (first < c.len)
-      hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kReduceThreads), 0, s, cp, c.nchunks, first,
-                         c.len, c.out, c.own, prio, c.trace);
+    if (tail)
+      hipLaunchKernelGGL(reduce_scalar_kernel, dim3(1), dim3(kReduceThreads), 0, s, cp, c.nchunks, nvec * 4,
+                         c.len, c.out, c.own, prio, tr);
   } else {
-    hipLaunchKernelGGL(reduce_scalar_kernel, dim3(clamp_wgs(c.len, wgs, kReduceThreads)), dim3(kReduceThreads), 0, s, cp,
-                       c.nchunks, (size_t)0, c.len, c.out, c.own, prio, c.trace);
+    const int g = clamp_wgs(c.len, wgs, kReduceThreads);
+    if (tr.wait != nullptr) tr.ack_target = (uint32_t)g;
+    hipLaunchKernelGGL(reduce_scalar_kernel, dim3(g), dim3(kReduceThreads), 0, s, cp,
+                       c.nchunks, (size_t)0, c.len, c.out, c.own, prio, tr);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }
@@ -347,25 +353,28 @@ int permute_launch(const PermuteCall &c, hipStream_t s) {
   memset(&pt, 0, sizeof pt);
   for (int i = 0; i < c.nchunks; ++i) pt.p[i] = c.perm[i];
   int wgs = c.wgs > 0 ? c.wgs : permute_default_wgs(c);
+  KHooks tr = c.trace;
   if (aligned16(c.src) && aligned16(c.dst) && c.chunk_bytes % 16 == 0) {
     int parts = permute_parts(c.chunk_bytes);
     long long items = (long long)c.nchunks * parts;
     int g = (int)(wgs < items ? wgs : items);
+    if (tr.wait != nullptr) tr.ack_target = (uint32_t)g;
     const uint32_t pace = pace_ticks((double)g * kPermuteThreads * kPermuteUnroll * 16.0 * 2.0, c.rate_gbs);
     // 32-bit offsets when a chunk plus one unrolled block stays below 2^32 bytes
     if ((double)c.chunk_bytes + (double)kPermuteUnroll * kPermuteThreads * 16.0 < 4294967296.0)
       hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, true>), dim3(g), dim3(kPermuteThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
-                         c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
+                         c.chunk_bytes / 16, parts, c.priority, pace, tr);
     else
       hipLaunchKernelGGL((permute_vec_kernel<kPermuteUnroll, false>), dim3(g), dim3(kPermuteThreads), 0, s,
                          static_cast<const u32x4 *>(c.src), static_cast<u32x4 *>(c.dst), pt, c.nchunks,
-                         c.chunk_bytes / 16, parts, c.priority, pace, c.trace);
+                         c.chunk_bytes / 16, parts, c.priority, pace, tr);
   } else {
     int g = clamp_wgs(c.chunk_bytes, wgs, kPermuteThreads);
+    if (tr.wait != nullptr) tr.ack_target = (uint32_t)g;
     hipLaunchKernelGGL(permute_byte_kernel, dim3(g), dim3(kPermuteThreads), 0, s,
                        static_cast<const uint8_t *>(c.src), static_cast<uint8_t *>(c.dst), pt,
-                       c.nchunks, c.chunk_bytes, c.priority, c.trace);
+                       c.nchunks, c.chunk_bytes, c.priority, tr);
   }
   return hipGetLastError() == hipSuccess ? OCC_OK : OCC_EHIP;
 }

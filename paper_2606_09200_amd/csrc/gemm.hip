@@ -1,19 +1,21 @@
-// K_g: bf16 GEMM C = A * B^T on MFMA (gfx950), fp32 accumulation, bf16 output.
+// K_g: bf16 GEMM on MFMA (gfx950), fp32 accumulation, bf16 output.
 //
-// Background, item 1: the GEMM of a linear layer, tiled and staged through
-// on-chip memory.  Section 3.1: the LDS a workgroup allocates,
+// Background, item 1: C = A * B, the GEMM of a linear layer, tiled and staged
+// through on-chip memory.  Section 3.1: the LDS a workgroup allocates,
 // S_blk ~ TILE_M*TILE_K + TILE_K*TILE_N, bounds how many GEMM workgroups
 // reside on a CU; an extra dynamic-LDS pad on top of the tile's own LDS lowers
 // that residency without changing the kernel's arithmetic.
 //
-// Layout: A is M x K, B is N x K (both K-contiguous, so both MFMA operands are
-// read from LDS as 16-byte rows), C is M x N, all row-major.
+// Layout: A is M x K and C is M x N, row-major.  B is stored K x N (occ_gemm:
+// C = A * B, the B tile is staged as stored and read with LDS transpose
+// reads) or N x K (occ_gemm_bt: C = A * B^T, a linear layer's weight layout,
+// both MFMA operands read from LDS as 16-byte rows).
 //
-// The kernels live in gemm_tiled.h (register-staged tiles, the paper's
-// opt1/opt2), gemm_dl.h (direct-to-LDS tiles, the default for large shapes),
-// gemm_skinny.h and gemm_skinny_ldsb.h (M <= 16) and gemm_skinny_kn.h
-// (M <= 16, B stored K x N); this file holds the variant table, the launch
-// plan and the launcher.
+// The kernels live in gemm_dl.h (direct-to-LDS tiles, both layouts),
+// gemm_tiled.h (register-staged tiles, the paper's opt1/opt2 with B N x K),
+// gemm_skinny.h and gemm_skinny_ldsb.h (M <= 16, B N x K) and
+// gemm_skinny_kn.h (M <= 16, B K x N); this file holds the variant table, the
+// launch plan and the launcher.
 #include "gemm_dl.h"
 #include "gemm_skinny.h"
 #include "gemm_skinny_kn.h"
@@ -28,9 +30,9 @@ namespace {
 // ---------------------------------------------------------------------------
 // Variant table.
 typedef void (*TiledFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, int,
-                        int, KTrace);
+                        int, KHooks);
 
-typedef void (*SkinnyFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, KTrace);
+typedef void (*SkinnyFn)(const uint16_t *, const uint16_t *, uint16_t *, int, int, int, int, KHooks);
 
 struct Variant {
   int id;
@@ -77,13 +79,6 @@ constexpr Variant make_skinny_variant(int id, const char *name) {
                  gemm_skinny_kernel<WAVES, UNROLL>, name, 0, 0, false, 0};
 }
 
-template <int WAVES, int KBW, int UNROLL>
-constexpr Variant make_skinny_areg_variant(int id, const char *name) {
-  return Variant{id, 16, 16, kSkinnyKB * UNROLL, 64 * WAVES, 2 * (WAVES - 1) * 64 * 16, nullptr,
-                 gemm_skinny_areg_kernel<WAVES, KBW, UNROLL>, name, WAVES * KBW * kSkinnyKB,
-                 2 * WAVES * kSkinnyKB * UNROLL, false, 0};
-}
-
 // A K x N B block (32 rows of N) is addressed with 32-bit offsets from its
 // first row (columns past N marked with 2^31), an A row (M <= 16 rows of K)
 // likewise from A.
@@ -102,77 +97,44 @@ constexpr Variant make_skinny_ldsb_variant(int id, const char *name) {
                  gemm_skinny_ldsb_kernel<WAVES, STAGES, KBW>, name, 32 * WAVES * KBW, kSlbKB * WAVES, false, 0, 1};
 }
 
-using T256x256_4w = Tile<256, 256, 64, 2, 2, 2>;
-using T256x256_8w = Tile<256, 256, 64, 2, 4, 2>;
-using T256x128_4w = Tile<256, 128, 64, 2, 2, 2>;
-using T256x128_4w_1s = Tile<256, 128, 64, 2, 2, 1>;
-using T128x128_4w = Tile<128, 128, 64, 2, 2, 2>;
+// B stored N x K (occ_gemm_bt)
 using T64x64_opt1 = Tile<64, 64, 32, 2, 2, 1>;   // Table 1 opt1: 64x64x32
 using T64x64_opt2 = Tile<64, 64, 64, 2, 2, 1>;   // Table 1 opt2: 64x64x64
-using T256x256_k32_1s = Tile<256, 256, 32, 2, 2, 1>;
-using D256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2>;
-using D256x256k32_8w_4s = Tile<256, 256, 32, 2, 4, 4>;
-using D256x256k32_8w_3s = Tile<256, 256, 32, 2, 4, 3>;
-using D256x128_4w_3s = Tile<256, 128, 64, 2, 2, 3>;
 using D128x128_4w_3s = Tile<128, 128, 64, 2, 2, 3>;
-using D256x128_8w_3s = Tile<256, 128, 64, 4, 2, 3>;
 using P256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true>;
-using P256x256k32_8w_4s = Tile<256, 256, 32, 2, 4, 4, true>;
-using P256x128_4w_3s = Tile<256, 128, 64, 2, 2, 3, true>;
-using P256x256_4w_2s = Tile<256, 256, 64, 2, 2, 2, true>;
 // two workgroups per CU: each has its own barriers, so one computes while the
-// other waits (48-72 KiB of LDS, 4 waves of 128x64 each)
-using P256x128k32_4w_2s = Tile<256, 128, 32, 2, 2, 2, true, 2>;
+// other waits (48 KiB of LDS, 4 waves of 128x64 each)
 using P128x256k32_4w_2s = Tile<128, 256, 32, 1, 4, 2, true, 2>;
-using P256x128k32_4w_3s = Tile<256, 128, 32, 2, 2, 3, true, 2>;
-using P128x256k32_4w_3s = Tile<128, 256, 32, 1, 4, 3, true, 2>;
 
-// B stored K x N (transpose reads from LDS)
+// B stored K x N (occ_gemm): the same tiles with the B tile staged as stored
+// and its MFMA operands read with LDS transpose reads
 using PKN256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true, 1, true>;
-
-constexpr int kSkinnyId = 8;
+using KN128x128_4w_3s = Tile<128, 128, 64, 2, 2, 3, false, 1, true>;
+using KN64x64_opt1 = Tile<64, 64, 32, 2, 2, 1, false, 1, true>;   // Table 1 opt1, one stage
+using KN64x64_opt2 = Tile<64, 64, 64, 2, 2, 1, false, 1, true>;   // Table 1 opt2, one stage
+using PKN128x256k32_4w_2s = Tile<128, 256, 32, 1, 4, 2, true, 2, true>;
 
 const Variant kVariants[] = {
-    make_variant<T256x256_4w>(1, "256x256x64 4w 2st"),
-    make_variant<T256x256_8w>(2, "256x256x64 8w 2st"),
-    make_variant<T256x128_4w>(3, "256x128x64 4w 2st"),
-    make_variant<T256x128_4w_1s>(4, "256x128x64 4w 1st"),
-    make_variant<T128x128_4w>(5, "128x128x64 4w 2st"),
-    make_variant<T64x64_opt1>(6, "64x64x32 opt1"),
-    make_variant<T64x64_opt2>(7, "64x64x64 opt2"),
-    make_skinny_variant<4, 16>(kSkinnyId, "skinny M<=16, 4 waves"),
-    make_variant<T256x256_k32_1s>(9, "256x256x32 4w 1st"),
-    make_dl_variant<D256x256_8w_2s>(10, "dl 256x256x64 8w 2st"),
-    make_dl_variant<D256x256k32_8w_4s>(11, "dl 256x256x32 8w 4st"),
-    make_dl_variant<D256x256k32_8w_3s>(12, "dl 256x256x32 8w 3st"),
-    make_dl_variant<D256x128_4w_3s>(13, "dl 256x128x64 4w 3st"),
-    make_dl_variant<D128x128_4w_3s>(14, "dl 128x128x64 4w 3st"),
-    make_dl_variant<D256x128_8w_3s>(15, "dl 256x128x64 8w 3st"),
-    make_dl_variant<P256x256_8w_2s>(16, "dl+pipe 256x256x64 8w 2st"),
-    make_dl_variant<P256x256k32_8w_4s>(17, "dl+pipe 256x256x32 8w 4st"),
-    make_dl_variant<P256x128_4w_3s>(18, "dl+pipe 256x128x64 4w 3st"),
-    make_dl_variant<P256x256_4w_2s>(19, "dl+pipe 256x256x64 4w 2st"),
-    make_skinny_variant<8, 16>(20, "skinny M<=16, 8 waves"),
-    make_skinny_variant<8, 8>(21, "skinny M<=16, 8 waves, unroll 8"),
-    make_skinny_variant<4, 8>(22, "skinny M<=16, 4 waves, unroll 8"),
-    make_skinny_variant<16, 8>(23, "skinny M<=16, 16 waves, unroll 8"),
-    make_dl_variant<P256x128k32_4w_2s>(24, "dl+pipe 256x128x32 4w 2st"),
-    make_dl_variant<P128x256k32_4w_2s>(25, "dl+pipe 128x256x32 4w 2st"),
-    make_dl_variant<P256x128k32_4w_3s>(26, "dl+pipe 256x128x32 4w 3st"),
-    make_dl_variant<P128x256k32_4w_3s>(27, "dl+pipe 128x256x32 4w 3st"),
-    make_skinny_areg_variant<8, 32, 4>(28, "skinny M<=16, A in registers, 8 waves, K<=8192, K%2048==0"),
-    make_skinny_areg_variant<8, 16, 4>(29, "skinny M<=16, A in registers, 8 waves, K<=4096, K%2048==0"),
+    // B stored N x K
+    make_variant<T64x64_opt1>(6, "64x64x32 opt1, B N x K"),
+    make_variant<T64x64_opt2>(7, "64x64x64 opt2, B N x K"),
+    make_dl_variant<D128x128_4w_3s>(14, "dl 128x128x64 4w 3st, B N x K"),
+    make_dl_variant<P256x256_8w_2s>(16, "dl+pipe 256x256x64 8w 2st, B N x K"),
+    make_skinny_variant<8, 8>(21, "skinny M<=16, 8 waves, unroll 8, B N x K"),
+    make_dl_variant<P128x256k32_4w_2s>(25, "dl+pipe 128x256x32 4w 2st 2wg/cu, B N x K"),
+    make_skinny_ldsb_variant<8, 2, 32>(34, "skinny M<=16, B via LDS in 256-byte row pieces, A in registers, 8 waves, K<=8192, K%1024==0, B N x K"),
+    // B stored K x N
     make_dl_variant<PKN256x256_8w_2s>(32, "dl+pipe 256x256x64 8w 2st, B K x N"),
-    make_skinny_kn_variant<4, 2, 128>(33, "skinny M<=16, B K x N, 128-column units, 4 waves, 2 LDS stages"),
-    make_skinny_ldsb_variant<8, 2, 32>(34, "skinny M<=16, B via LDS in 256-byte row pieces, A in registers, 8 waves, K<=8192, K%1024==0"),
+    make_skinny_kn_variant<4, 2, 128>(33, "skinny M<=16, 128-column units, 4 waves, 2 LDS stages, B K x N"),
+    make_dl_variant<KN128x128_4w_3s>(35, "dl 128x128x64 4w 3st, B K x N"),
+    make_dl_variant<KN64x64_opt1>(36, "dl 64x64x32 opt1 1st, B K x N"),
+    make_dl_variant<KN64x64_opt2>(37, "dl 64x64x64 opt2 1st, B K x N"),
+    make_dl_variant<PKN128x256k32_4w_2s>(38, "dl+pipe 128x256x32 4w 2st 2wg/cu, B K x N"),
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
-
-constexpr int kKnVariant = 32;        // the K x N B kernel
-constexpr int kKnSkinnyVariant = 33;  // the K x N B kernel for M <= 16
 
 const Variant *find_variant(int id) {
   for (const Variant &v : kVariants)
@@ -182,20 +144,25 @@ const Variant *find_variant(int id) {
 
 int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
-int auto_variant(int M, int N, int K, int num_cus) {
+// The kernel for a shape: skinny for M <= 16, else the largest tile that
+// still gives at least one 256x256 tile per CU (or one 128x128 tile per two
+// CUs), else the paper's opt2 64x64x64 tile.  A K beyond what a direct-to-LDS
+// tile addresses with 32-bit offsets takes the 64x64 tile.
+int auto_variant(int M, int N, int K, int num_cus, bool b_kn) {
   if (M <= 16) {
-    // skinny, 8 waves; A kept in registers and B staged through LDS when K
-    // is whole 1024-wide slices that fit, else 8 k-blocks of A and B in
-    // flight per lane
+    if (b_kn) return 33;
+    // A kept in registers and B staged through LDS when K is whole
+    // 1024-wide slices that fit, else 8 k-blocks of A and B in flight per lane
     if (K >= 1024 && K % 1024 == 0 && K <= 8192) return 34;
     return 21;
   }
+  const int large = b_kn ? 32 : 16, mid = b_kn ? 35 : 14, small = b_kn ? 37 : 7;
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
-  if (big >= num_cus) return K <= find_variant(16)->kmax ? 16 : 3;  // 3: 64-bit addressing
-  long long mid = (long long)ceil_div(M, 128) * ceil_div(N, 128);
-  // 128x128 tiles through three direct-to-LDS stages (5: 64-bit addressing)
-  if (mid >= num_cus / 2) return K <= find_variant(14)->kmax ? 14 : 5;
-  return 7;
+  long long mids = (long long)ceil_div(M, 128) * ceil_div(N, 128);
+  int v = big >= num_cus ? large : (mids >= num_cus / 2 ? mid : small);
+  const Variant *pv = find_variant(v);
+  if (pv->kmax > 0 && K > pv->kmax) v = small;
+  return v;
 }
 
 }  // namespace
@@ -236,16 +203,22 @@ static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_g
   return OCC_OK;
 }
 
-int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
+// The launch plan without the occupancy figure: all a launch needs (the
+// occupancy query costs host time on every call, which launch-bound
+// schedules cannot spare).
+static int launch_plan(const GemmCall &c, occ_gemm_plan *plan) {
   const DeviceInfo *di = nullptr;
   int st = current_device_info(&di);
   if (st != OCC_OK) return st;
   int variant = c.variant;
-  if (variant == 0)
-    variant = c.b_kn ? (c.M <= 16 ? kKnSkinnyVariant : kKnVariant) : auto_variant(c.M, c.N, c.K, di->num_cus);
-  st = fill_plan(c, variant, *di, plan);
+  if (variant == 0) variant = auto_variant(c.M, c.N, c.K, di->num_cus, c.b_kn);
+  return fill_plan(c, variant, *di, plan);
+}
+
+int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
+  int st = launch_plan(c, plan);
   if (st != OCC_OK) return st;
-  const Variant *v = find_variant(variant);
+  const Variant *v = find_variant(plan->kernel_id);
   int dyn = (int)(v->fn ? v->lds + c.lds_bytes : c.lds_bytes);
   int nb = 0;
   hipError_t e = v->fn ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, v->fn, v->threads, dyn)
@@ -257,7 +230,7 @@ int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
 
 int gemm_launch(const GemmCall &c, hipStream_t s) {
   occ_gemm_plan p;
-  int st = gemm_plan(c, &p);
+  int st = launch_plan(c, &p);
   if (st != OCC_OK) return st;
   if (c.M == 0 || c.N == 0) return OCC_OK;
   const Variant *v = find_variant(p.kernel_id);

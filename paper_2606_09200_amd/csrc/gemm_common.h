@@ -50,7 +50,8 @@ struct Tile {
   static_assert(KCH == 4 || KCH == 8, "BK must be 32 or 64");
   static_assert(A_LOADS >= 1 && B_LOADS >= 1, "tile too small for the workgroup");
   static_assert(BM % ROWS_PER_PASS == 0, "uneven load passes");
-  static_assert(BKN ? (BK % B_RPP == 0 && B_RPP % 4 == 0 && BCH >= 16) : (BN % ROWS_PER_PASS == 0),
+  static_assert(BKN ? (BK % B_RPP == 0 && B_RPP % 4 == 0 && (BCH >= 16 || BCH == 8))
+                    : (BN % ROWS_PER_PASS == 0),
                 "uneven load passes");
 };
 
@@ -67,13 +68,19 @@ __device__ __forceinline__ int swz(int r, int c) {
   else return c ^ ((r >> 2) & 3);
 }
 
-// Physical 16-byte chunk of logical chunk c in row k of a K x N B tile.  A
-// transpose read sends, per 16 lanes, 4 consecutive rows at one 32-byte
-// column piece (per 32 lanes: 4 rows x 64 bytes); rows are BN*2 bytes, a
-// multiple of 256, so all 4 rows would hit the same banks.  XOR-ing the chunk
-// with 4*(k % 4) moves the 4 rows' 64-byte pieces to 4 different 64-byte
-// quarters of the bank line.
-__device__ __forceinline__ int swz_kn(int k, int c) { return c ^ ((k & 3) << 2); }
+// Physical 16-byte chunk of logical chunk c in row k of a K x N B tile
+// (BCH chunks per row).  A transpose read sends, per 32 lanes, 4 consecutive
+// rows at one 64-byte column piece.  Rows of BN*2 >= 256 bytes (BCH >= 16)
+// would all hit the same banks: XOR-ing the chunk with 4*(k % 4) moves the 4
+// pieces to 4 different 64-byte quarters of the bank line.  Rows of 128 bytes
+// (BCH == 8, a 64-column tile) pair up in one bank line, so rows k and k+2
+// collide: XOR-ing the chunk with 4 for the second pair of the group swaps
+// its two 64-byte halves, and the 4 pieces again fill 4 different quarters.
+template <int BCH>
+__device__ __forceinline__ int swz_kn(int k, int c) {
+  if constexpr (BCH >= 16) return c ^ ((k & 3) << 2);
+  else return c ^ ((k & 2) << 1);
+}
 
 // XCD-aware order: dispatch hands consecutive workgroups to the 8 XCDs in
 // turn, so tile ids are regrouped to give each XCD a contiguous run of the

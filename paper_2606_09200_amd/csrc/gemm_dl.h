@@ -67,10 +67,10 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
                                                         const uint16_t *__restrict__ B,
                                                         uint16_t *__restrict__ C, int M, int N,
                                                         int K, int tiles_m, int tiles_n, int prio,
-                                                        KTrace tr) {
+                                                        KHooks tr) {
   extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   constexpr int S = T::STAGES;
   constexpr int PER_STAGE = T::A_LOADS + T::B_LOADS;
   static_assert(T::ROWS_PER_PASS % 16 == 0, "a lane's swizzle must not change between passes");
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
   // physical chunk qB; passes start at multiples of 4 rows, so the logical
   // chunk qB ^ swz is the same in every pass.
   const int rB = threadIdx.x / T::BCH;
-  const int cB = swz_kn(rB, threadIdx.x % T::BCH);
+  const int cB = swz_kn<T::BCH>(rB, threadIdx.x % T::BCH);
   // K x N B fragment reads (transpose reads, see below): within each group of
   // 16 lanes, lane s reads 4 consecutive columns at row (s / 4) of a 4-row
   // block; the hardware hands lane i of the group element j of lane
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
       if constexpr (T::BKN) {
         const int kr = ks * 16 + tr_k;
         const int n = wn * T::TN + j * 32 + tr_n;
-        const int off = swz_kn(kr, n >> 3) * 16 + (n & 7) * 2;
+        const int off = swz_kn<T::BCH>(kr, n >> 3) * 16 + (n & 7) * 2;
         const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) i16x4 *)(bs + kr * T::BROW_BYTES + off));
         const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -202,9 +202,19 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
     for (int kt = 0; kt < nk; ++kt) {
       // k-step kt has landed once at most min(S-2, nk-1-kt) later steps are
       // outstanding; the barrier then publishes it and retires step kt-1.
-      wait_stages<S - 2, PER_STAGE>(min(S - 2, nk - 1 - kt));
-      __syncthreads();
-      if (kt + S - 1 < nk) issue(kt + S - 1);
+      if constexpr (S == 1) {
+        // one stage (the paper's tile configurations): every wave is done
+        // with the previous k-step before the DMA overwrites it, and the
+        // k-step has landed for every wave before any reads it
+        __syncthreads();
+        issue(kt);
+        wait_vmcnt<0>();
+        __syncthreads();
+      } else {
+        wait_stages<S - 2, PER_STAGE>(min(S - 2, nk - 1 - kt));
+        __syncthreads();
+        if (kt + S - 1 < nk) issue(kt + S - 1);
+      }
 
       // Fragments of 16-wide k-substep ks+1 are read from LDS while the MFMAs
       // of substep ks run (two register sets); the scheduling groups below
@@ -253,7 +263,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
       }
     }
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 }  // namespace

@@ -81,14 +81,14 @@ template <int WAVES, int STAGES, int COLS>
 __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kn_kernel(const uint16_t *__restrict__ A,
                                                                     const uint16_t *__restrict__ B,
                                                                     uint16_t *__restrict__ C, int M,
-                                                                    int N, int K, int prio, KTrace tr) {
+                                                                    int N, int K, int prio, KHooks tr) {
   using G = SkinnyKn<WAVES, STAGES, COLS>;
   constexpr int S = STAGES;
   __shared__ __align__(16) unsigned char ring[G::LDS_BYTES];
   extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
   (void)pad_lds;
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar loop control
   const int nblk = (K + kSknKB - 1) / kSknKB;
@@ -202,7 +202,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_kn_kernel(const uint16
     }
     __syncthreads();  // the rings are refilled by the next unit
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 }  // namespace

@@ -45,7 +45,7 @@ template <int WAVES, int STAGES, int KBW>
 __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_ldsb_kernel(const uint16_t *__restrict__ A,
                                                                       const uint16_t *__restrict__ B,
                                                                       uint16_t *__restrict__ C, int M,
-                                                                      int N, int K, int prio, KTrace tr) {
+                                                                      int N, int K, int prio, KHooks tr) {
   using G = SkinnyLdsB<WAVES, STAGES, KBW>;
   constexpr int S = STAGES;
   constexpr int NBW = KBW / 4;  // most blocks per wave and unit
@@ -54,7 +54,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_ldsb_kernel(const uint
   extern __shared__ __align__(16) unsigned char pad_lds[];  // occupancy pad only
   (void)pad_lds;
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar loop control
   const int r = lane & 15;
@@ -156,7 +156,7 @@ __global__ __launch_bounds__(64 * WAVES) void gemm_skinny_ldsb_kernel(const uint
       }
     }
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 }  // namespace

@@ -56,10 +56,10 @@ __global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__res
                                                            const uint16_t *__restrict__ B,
                                                            uint16_t *__restrict__ C, int M, int N,
                                                            int K, int tiles_m, int tiles_n,
-                                                           int prio, KTrace tr) {
+                                                           int prio, KHooks tr) {
   extern __shared__ __align__(16) unsigned char smem[];  // tile stages, then the unused pad
   set_wave_priority(prio);
-  const TraceStart t0 = trace_begin(tr);
+  const HookStart t0 = hooks_begin(tr);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / T::WN;
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(T::NT) void gemm_tiled_kernel(const uint16_t *__res
       }
     }
   }
-  trace_end(tr, t0);
+  hooks_end(tr, t0);
 }
 
 }  // namespace

@@ -35,8 +35,8 @@ struct GemmCall {
   int grid_cap;         // 0 = one workgroup per tile
   int variant;          // 0 = automatic, else a kernel variant id
   int priority;         // wave priority 0..3 (s_setprio)
-  KTrace trace;         // optional tracing (all null = off)
-  bool b_kn = false;    // B stored K x N (C = A B) instead of N x K (C = A B^T)
+  KHooks trace;         // per-launch hooks: tracing, dependency counter (all off by default)
+  bool b_kn = false;    // B stored K x N (occ_gemm: C = A B) or N x K (occ_gemm_bt: C = A B^T)
 };
 int gemm_plan(const GemmCall &c, occ_gemm_plan *plan);
 bool gemm_variant_is_kn(int id);  // a variant that takes B stored K x N
@@ -50,7 +50,7 @@ struct ReduceCall {
   float *out;
   int wgs;                   // 0 = default
   int priority;              // 0..3
-  KTrace trace;
+  KHooks trace;
   double rate_gbs;           // target bandwidth of the vector path, GB/s; 0 = unpaced
   // when set: the first term of every sum is this bf16 buffer, widened to
   // binary32, and bufs holds the nchunks (>= 0) fp32 terms after it
@@ -67,7 +67,7 @@ struct PermuteCall {
   size_t chunk_bytes;
   int wgs;
   int priority;
-  KTrace trace;
+  KHooks trace;
   double rate_gbs;           // as ReduceCall::rate_gbs
 };
 int permute_launch(const PermuteCall &c, hipStream_t s);

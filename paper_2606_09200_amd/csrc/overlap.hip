@@ -2,11 +2,13 @@
 // GEMM -> collective iterations (Section 3.2, Fig. 1).
 //
 //   SEQ: one stream, G0 C0 G1 C1 ... G_{n-1} C_{n-1}.
-//   OVL: G_i on the compute stream; an event recorded after G_i is waited on
-//        by the comm stream before C_i (K_g^i -> K_c^i, Section 3.3), so
-//        G_{i+1} may run while C_i does.  The collective's precedence over
-//        later GEMMs is the comm kernel's wave priority (s_setprio); both
-//        streams keep the default queue priority.
+//   OVL: G_i on the compute stream, C_i on the comm stream after G_i
+//        (K_g^i -> K_c^i), so G_{i+1} may run while C_i does.  The edge is an
+//        event recorded after G_i and waited on before C_i (OCC_DEP_EVENT),
+//        or a device-side counter that G_i's workgroups count up and C_i's
+//        workgroups wait on (OCC_DEP_COUNTER).  The collective's precedence
+//        over later GEMMs is the comm kernel's wave priority (s_setprio);
+//        both streams keep the default queue priority.
 //   ISO: SEQ with an event between every two kernels, giving the mean
 //        duration of one GEMM and of one collective launch.
 //
@@ -56,6 +58,30 @@ struct Events {
   }
 };
 
+// Per-device buffer of the counter dependency: kMaxDepIter counters of
+// finished GEMM workgroups (one per iteration), kMaxDepIter counters of
+// collective workgroups past their wait, and one error word.  Allocated and
+// zeroed once per device; every complete schedule leaves it zeroed again.
+constexpr int kMaxDepIter = 1024;
+constexpr size_t kDepWords = 2 * kMaxDepIter + 64;
+uint32_t *g_dep[64];
+
+int dep_scratch(uint32_t **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OCC_ENODEV;
+  if (g_dep[dev] == nullptr) {
+    void *p = nullptr;
+    if (hipMalloc(&p, kDepWords * sizeof(uint32_t)) != hipSuccess) return OCC_EHIP;
+    if (hipMemset(p, 0, kDepWords * sizeof(uint32_t)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+      (void)hipFree(p);
+      return OCC_EHIP;
+    }
+    g_dep[dev] = static_cast<uint32_t *>(p);
+  }
+  *out = g_dep[dev];
+  return OCC_OK;
+}
+
 #define OCC_TRY(x)                 \
   do {                             \
     int st_ = (x);                 \
@@ -76,7 +102,7 @@ struct Launcher {
   // iteration i's collective reduces as its first term
   bool own = false;
   void *c_iter(int i) const { return static_cast<uint16_t *>(g.C) + (own ? (size_t)i * g.M * g.N : 0); }
-  int gemm(hipStream_t s, KTrace t, int i) {
+  int gemm(hipStream_t s, KHooks t, int i) {
     GemmCall c = g;
     c.C = c_iter(i);
     c.trace = t;
@@ -86,7 +112,7 @@ struct Launcher {
   // sequential schedule and the isolated timings do too when pace_all.
   double rate_gbs;
   bool pace_all;
-  int comm(hipStream_t s, KTrace t, bool paced, int i) {
+  int comm(hipStream_t s, KHooks t, bool paced, int i) {
     paced = paced || pace_all;
     if (kind == OCC_COMM_REDUCE || kind == OCC_COMM_REDUCE_OWN) {
       ReduceCall c = r;
@@ -113,8 +139,14 @@ int validate_cfg(const occ_overlap_cfg *c) {
   if (c->wg_trace != nullptr && c->wg_trace_cap < 0) return OCC_EINVAL;
   if (!(c->comm_rate_gbs == 0.0 || (c->comm_rate_gbs >= OCC_MIN_COMM_RATE_GBS && c->comm_rate_gbs <= 1.0e6)))
     return OCC_EINVAL;
-  if (c->gemm_b_layout != 0 && c->gemm_b_layout != 1) return OCC_EINVAL;
-  OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K, c->gemm_b_layout == 1));
+  if (c->gemm_b_layout != OCC_B_KN && c->gemm_b_layout != OCC_B_NK) return OCC_EINVAL;
+  if (c->dep != OCC_DEP_EVENT && c->dep != OCC_DEP_COUNTER) return OCC_EINVAL;
+  if (c->dep == OCC_DEP_COUNTER && c->n_iter > kMaxDepIter) return OCC_EINVAL;
+  // a replayed graph may run its two branches on one queue in any
+  // topological order; a collective placed before its GEMM would then wait
+  // out its whole bound, so graphs keep the event dependency
+  if (c->dep == OCC_DEP_COUNTER && (c->flags & OCC_RUN_GRAPH)) return OCC_EINVAL;
+  OCC_TRY(validate_gemm(c->A, c->B, c->C, c->M, c->N, c->K, c->gemm_b_layout == OCC_B_KN));
   size_t cbytes = (size_t)c->M * c->N * 2;
   // K_g writes C while K_c runs: C must not overlap anything K_c touches,
   // and K_c's output must not overlap A or B.
@@ -162,7 +194,7 @@ namespace {
 // The two schedules, enqueued without timing events (so that they can also be
 // captured into a graph).  OVL forks the comm stream off the compute stream
 // and joins it back, so the compute stream's next operation follows both.
-int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KTrace &off) {
+int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KHooks &off) {
   for (int i = 0; i < n; ++i) {
     OCC_TRY(L.gemm(s0, off, i));
     OCC_TRY(L.comm(s0, off, false, i));
@@ -171,13 +203,16 @@ int enqueue_seq(Launcher &L, hipStream_t s0, int n, const KTrace &off) {
 }
 
 int enqueue_ovl(Launcher &L, hipStream_t s0, hipStream_t s1, hipEvent_t fork, hipEvent_t *deps,
-                hipEvent_t join, int n, const KTrace *tg, const KTrace *tc) {
+                hipEvent_t join, int n, const KHooks *tg, const KHooks *tc, bool counter) {
   OCC_HIP(hipEventRecord(fork, s0));
   OCC_HIP(hipStreamWaitEvent(s1, fork, 0));
   for (int i = 0; i < n; ++i) {
     OCC_TRY(L.gemm(s0, tg[i], i));
-    OCC_HIP(hipEventRecord(deps[i], s0));
-    OCC_HIP(hipStreamWaitEvent(s1, deps[i], 0));
+    if (!counter) {
+      OCC_HIP(hipEventRecord(deps[i], s0));
+      OCC_HIP(hipStreamWaitEvent(s1, deps[i], 0));
+    }
+    // (with the counter, tg[i] and tc[i] carry the edge to the device)
     OCC_TRY(L.comm(s1, tc[i], true, i));
   }
   // C_{n-1} waits on G_{n-1}, the last GEMM, so the comm stream's end is the
@@ -228,9 +263,9 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
 
   Launcher L;
   L.kind = c.comm_kind;
-  const KTrace off{nullptr, nullptr, 0, 0};
+  const KHooks off{};
   L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
-                 c.gemm_priority, off, c.gemm_b_layout == 1};
+                 c.gemm_priority, off, c.gemm_b_layout == OCC_B_KN};
   L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
   L.own = c.comm_kind == OCC_COMM_REDUCE_OWN;
   if (L.own) L.r.own = static_cast<const uint16_t *>(c.C);
@@ -246,6 +281,20 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   res->comm_wgs = c.comm_wgs > 0 ? c.comm_wgs
                   : (c.comm_kind != OCC_COMM_PERMUTE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
 
+  // The counter dependency: every collective workgroup may wait on a CU
+  // beside the GEMM, so at most one per CU (then some CU always has room for
+  // a GEMM workgroup and the GEMM cannot be starved by waiting workgroups).
+  const bool counter = c.dep == OCC_DEP_COUNTER;
+  uint32_t *dep = nullptr;
+  if (counter) {
+    const DeviceInfo *di = nullptr;
+    OCC_TRY(current_device_info(&di));
+    if (res->comm_wgs > di->num_cus) return OCC_EINVAL;
+    // a collective that launches nothing would leave its counter counted up
+    if ((c.comm_kind == OCC_COMM_PERMUTE ? c.chunk_bytes : c.len) == 0) return OCC_EINVAL;
+    OCC_TRY(dep_scratch(&dep));
+  }
+
   StreamPair *sp = nullptr;
   OCC_TRY(stream_pair(&sp));
   hipStream_t s0 = sp->comp, s1 = sp->comm;
@@ -253,10 +302,35 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   Events timing, deps, marks;
   OCC_TRY(timing.make(2 * n + 5, hipEventDefault));
   OCC_TRY(deps.make(n, hipEventDisableTiming));
-  OCC_TRY(marks.make(2, hipEventDisableTiming));  // fork, join
+  OCC_TRY(marks.make(3, hipEventDisableTiming));  // fork, join, caller
   hipEvent_t *ev = timing.ev.data();
   hipEvent_t *iso = ev + 4;  // 2n+1 boundaries of the isolated pass
-  std::vector<KTrace> offs(n, off);
+
+  // Everything runs after the work already queued on the caller's stream
+  // (the comm stream forks off s0 in every overlapped schedule).
+  OCC_HIP(hipEventRecord(marks.ev[2], static_cast<hipStream_t>(c.stream)));
+  OCC_HIP(hipStreamWaitEvent(s0, marks.ev[2], 0));
+
+  // Per-iteration hooks of the overlapped schedule: none with the event
+  // dependency; with the counter, G_i counts its finished workgroups in
+  // dep[i] and C_i waits for all of them (then acknowledges in
+  // dep[kMaxDepIter + i]).  Stores and loads are ordered through the counter
+  // only when the collective reads the GEMM's output.
+  std::vector<KHooks> hg(n, off), hc(n, off);
+  if (counter) {
+    const uint32_t target = (c.M > 0 && c.N > 0) ? (uint32_t)plan.grid : 0u;
+    for (int i = 0; i < n; ++i) {
+      hg[i].signal = dep + i;
+      hg[i].release = L.own ? 1u : 0u;
+      hc[i].wait = dep + i;
+      hc[i].ack = dep + kMaxDepIter + i;
+      hc[i].err = dep + 2 * kMaxDepIter;
+      hc[i].wait_target = target;
+      hc[i].acquire = L.own ? 1u : 0u;
+    }
+    // every counter at zero (a call that failed half-way may have left some)
+    OCC_HIP(hipMemsetAsync(dep, 0, kDepWords * sizeof(uint32_t), s0));
+  }
 
   // Graph mode: capture each schedule once, replay it per repetition.
   Graph gseq, govl;
@@ -270,8 +344,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     }
     if (flags & OCC_RUN_OVL) {
       OCC_HIP(hipStreamBeginCapture(s0, hipStreamCaptureModeRelaxed));
-      int st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, offs.data(),
-                           offs.data());
+      int st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, hg.data(), hc.data(),
+                           counter);
       int st2 = govl.end_capture(s0);
       OCC_TRY(st);
       OCC_TRY(st2);
@@ -301,8 +375,8 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
     if (flags & OCC_RUN_OVL) {
       OCC_HIP(hipEventRecord(ev[2], s0));
       if (graph) st = hipGraphLaunch(govl.x, s0) == hipSuccess ? OCC_OK : OCC_EHIP;
-      else st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, offs.data(),
-                            offs.data());
+      else st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, hg.data(), hc.data(),
+                            counter);
       OCC_HIP(hipEventRecord(ev[3], s0));
       OCC_HIP(hipEventSynchronize(ev[3]));
       if (st != OCC_OK) break;
@@ -346,17 +420,34 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   // per workgroup (tag = 2*iteration + 0 for the GEMM, + 1 for the collective).
   if (c.timeline != nullptr || c.wg_trace != nullptr) {
     OCC_TRY(trace_reset(c.timeline, 2 * n, c.wg_trace, s0));
-    std::vector<KTrace> tg(n), tc(n);
+    std::vector<KHooks> tg(hg), tc(hc);
     for (int i = 0; i < n; ++i) {
-      tg[i] = KTrace{c.timeline ? c.timeline + 4 * i : nullptr, c.wg_trace, (uint32_t)c.wg_trace_cap,
-                     (uint32_t)(2 * i)};
-      tc[i] = KTrace{c.timeline ? c.timeline + 4 * i + 2 : nullptr, c.wg_trace,
-                     (uint32_t)c.wg_trace_cap, (uint32_t)(2 * i + 1)};
+      tg[i].stamps = c.timeline ? c.timeline + 4 * i : nullptr;
+      tg[i].wg = c.wg_trace;
+      tg[i].wg_cap = (uint32_t)c.wg_trace_cap;
+      tg[i].tag = (uint32_t)(2 * i);
+      tc[i].stamps = c.timeline ? c.timeline + 4 * i + 2 : nullptr;
+      tc[i].wg = c.wg_trace;
+      tc[i].wg_cap = (uint32_t)c.wg_trace_cap;
+      tc[i].tag = (uint32_t)(2 * i + 1);
     }
-    st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, tg.data(), tc.data());
+    st = enqueue_ovl(L, s0, s1, marks.ev[0], deps.ev.data(), marks.ev[1], n, tg.data(), tc.data(), counter);
     OCC_HIP(hipEventRecord(ev[3], s0));
     OCC_HIP(hipEventSynchronize(ev[3]));
     if (st != OCC_OK) return st;
+  }
+
+  // A collective workgroup whose bounded wait ran out: the schedule's
+  // ordering was not kept.  Leave the counters zeroed for the next call.
+  if (counter) {
+    uint32_t err = 0;
+    OCC_HIP(hipMemcpy(&err, dep + 2 * kMaxDepIter, sizeof err, hipMemcpyDeviceToHost));
+    if (err != 0) {
+      OCC_HIP(hipDeviceSynchronize());
+      OCC_HIP(hipMemset(dep, 0, kDepWords * sizeof(uint32_t)));
+      OCC_HIP(hipDeviceSynchronize());
+      return OCC_ETIMEOUT;
+    }
   }
 
   const double R = c.reps;
@@ -381,10 +472,12 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
 
 // Adaptive choice of the occupancy and priority knobs (the runtime policy the
 // paper names as future work, Section 6): time the overlapped schedule for
-// each candidate and keep the fastest.  Candidates: comm wave priority
-// {0, 3} x comm workgroups {one per CU (the default), two per CU} x GEMM grid {one
-// workgroup per tile, persistent one per CU} x extra LDS pad {0, the pad
-// that lowers the GEMM's residency by one workgroup per CU, when one exists}.
+// each candidate and keep the one with the shortest median makespan.
+// Candidates: comm wave priority {0, 3} x comm workgroups {one per CU (the
+// default), two per CU, one per four CUs} x GEMM grid {one workgroup per tile, persistent one
+// per CU} x extra LDS pad {0, the pad that lowers the GEMM's residency by one
+// workgroup per CU, when one exists} x dependency {event, device counter}
+// (the counter only with one comm workgroup per CU).
 int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                       int *prefer_sequential) {
   if (cfg == nullptr || res == nullptr || prefer_sequential == nullptr || tune_reps < 1)
@@ -398,7 +491,7 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   int npads = 1;
   {
     GemmCall g{cfg->A, cfg->B, cfg->C, cfg->M, cfg->N, cfg->K, 0, 0, cfg->gemm_variant,
-               cfg->gemm_priority, KTrace{nullptr, nullptr, 0, 0}, cfg->gemm_b_layout == 1};
+               cfg->gemm_priority, KHooks{}, cfg->gemm_b_layout == OCC_B_KN};
     occ_gemm_plan p0;
     OCC_TRY(gemm_plan(g, &p0));
     if (p0.wg_per_cu > 1) {
@@ -411,8 +504,11 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
     }
   }
   const int prios[2] = {0, 3};
-  const int wgs[2] = {0, 2 * di->num_cus};
+  // comm grids: one workgroup per CU (the default), two per CU, one per four
+  // CUs (a lightweight, low-occupancy collective)
+  const int wgs[3] = {0, 2 * di->num_cus, di->num_cus / 4 > 0 ? di->num_cus / 4 : 1};
   const int grids[2] = {0, di->num_cus};
+  const int deps[2] = {OCC_DEP_EVENT, OCC_DEP_COUNTER};
 
   occ_overlap_cfg c = *cfg;
   c.reps = tune_reps;
@@ -423,28 +519,34 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   double best = 1e300;
   occ_overlap_cfg best_cfg = c;
   for (int a = 0; a < 2; ++a)
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < 3; ++b)
       for (int d = 0; d < 2; ++d)
-        for (int e = 0; e < npads; ++e) {
-          c.comm_priority = prios[a];
-          c.comm_wgs = wgs[b];
-          c.gemm_grid = grids[d];
-          c.lds_bytes = pads[e];
-          occ_overlap_result r;
-          int st = run_overlap_impl(&c, &r);
-          if (st == OCC_ELDS) continue;
-          if (st != OCC_OK) return st;
-          if (r.t_ovl_ms < best) {
-            best = r.t_ovl_ms;
-            best_cfg = c;
+        for (int e = 0; e < npads; ++e)
+          for (int f = 0; f < 2; ++f) {
+            if (deps[f] == OCC_DEP_COUNTER &&
+                (wgs[b] > di->num_cus || cfg->n_iter > kMaxDepIter || (c.flags & OCC_RUN_GRAPH)))
+              continue;
+            c.comm_priority = prios[a];
+            c.comm_wgs = wgs[b];
+            c.gemm_grid = grids[d];
+            c.lds_bytes = pads[e];
+            c.dep = deps[f];
+            occ_overlap_result r;
+            int st = run_overlap_impl(&c, &r);
+            if (st == OCC_ELDS) continue;
+            if (st != OCC_OK) return st;
+            if (r.t_ovl_median_ms < best) {
+              best = r.t_ovl_median_ms;
+              best_cfg = c;
+            }
           }
-        }
   cfg->comm_priority = best_cfg.comm_priority;
   cfg->comm_wgs = best_cfg.comm_wgs;
   cfg->gemm_grid = best_cfg.gemm_grid;
   cfg->lds_bytes = best_cfg.lds_bytes;
+  cfg->dep = best_cfg.dep;
   OCC_TRY(run_overlap_impl(cfg, res));
-  *prefer_sequential = (res->t_seq_ms > 0 && res->t_ovl_ms > res->t_seq_ms) ? 1 : 0;
+  *prefer_sequential = (res->t_seq_median_ms > 0 && res->t_ovl_median_ms > res->t_seq_median_ms) ? 1 : 0;
   return OCC_OK;
 }
 

@@ -28,22 +28,22 @@ def main(argv=None):
     ap.add_argument("--launches", type=int, default=5)
     ap.add_argument("--pad-kib", type=int, default=0)
     ap.add_argument("--variant", type=int, default=0)
-    ap.add_argument("--b-layout", default="nk", choices=["nk", "kn"],
-                    help="B stored N x K (occ_gemm) or K x N (occ_gemm_kn)")
+    ap.add_argument("--b-layout", default="kn", choices=["kn", "nk"],
+                    help="B stored K x N (occ_gemm) or N x K (occ_gemm_bt)")
     ap.add_argument("--copy-mib", type=int, default=1024)
     ap.add_argument("--no-copy", action="store_true")
     a = ap.parse_args(argv)
     w = WORKLOADS[a.workload]
     dev = "cuda:0"
     if a.kernel in ("gemm", "torch_mm"):
-        A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=dev)
+        A, Bt = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_b=w.std_b, seed_b=w.seed_b, device=dev)
         C = torch.empty((w.M, w.N), device=dev, dtype=torch.bfloat16)
-        if a.b_layout == "kn":
-            B = B.t().contiguous()
+        B = Bt.t().contiguous() if a.b_layout == "kn" else Bt
+        del Bt
         if a.kernel == "gemm" and a.b_layout == "kn":
-            run = lambda: occ.occ_gemm_kn_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
-        elif a.kernel == "gemm":
             run = lambda: occ.occ_gemm_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
+        elif a.kernel == "gemm":
+            run = lambda: occ.occ_gemm_bt_ex(A, B, C, lds_bytes=a.pad_kib << 10, variant=a.variant)
         elif a.b_layout == "kn":
             run = lambda: torch.mm(A, B, out=C)
         else:

@@ -30,9 +30,11 @@ PEAK_TFLOPS = 2500.0
 PEAK_GBS = 8000.0
 
 
-def setup(w, dev):
-    A, B = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_a=w.std_a, std_b=w.std_b,
-                                seed_b=w.seed_b, device=dev)
+def setup(w, dev, b_layout="kn"):
+    A, Bt = inputs.gemm_operands(w.M, w.N, w.K, seed=0, std_a=w.std_a, std_b=w.std_b,
+                                 seed_b=w.seed_b, device=dev)
+    B = Bt.t().contiguous() if b_layout == "kn" else Bt   # the same op(B) in the chosen layout
+    del Bt
     if w.comm == "reduce_own":
         C = torch.empty((w.n_iter, w.M, w.N), device=dev, dtype=torch.bfloat16)
         comm = dict(bufs=inputs.reduce_chunks(w.nchunks, w.length, seed=1, device=dev),
@@ -49,9 +51,18 @@ def setup(w, dev):
     return A, B, C, comm
 
 
+# The tiles of the pad sweep and the thread-block-count study, per layout of
+# B: the default tile (128 KiB of LDS: only small pads fit) and tiles small
+# enough for the pad to set residency -- 128x256x32 (48 KiB, two per CU),
+# 128x128x64 (96 KiB, three stages) and the paper's opt2 64x64x64 -- and the
+# paper's two tiles (opt1 64x64x32, opt2 64x64x64).
+SWEEP_VARIANTS = {"kn": (0, 38, 35, 37), "nk": (0, 25, 14, 7)}
+BLOCK_VARIANTS = {"kn": (36, 37), "nk": (6, 7)}
+
+
 def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs):
     plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, pad, knobs.get("gemm_variant", 0), knobs.get("gemm_grid", 0),
-                                   b_layout=knobs.get("b_layout", "nk"))
+                                   b_layout=knobs.get("b_layout", "kn"))
     row = {"workload": w.name, "pad_kib": pad >> 10, "comm_priority": prio,
            "gemm_grid": plan["grid"],
            "gemm_variant": plan["kernel_id"], "gemm_tile_lds": plan["tile_lds_bytes"],
@@ -91,7 +102,7 @@ def measure(w, A, B, C, comm, pad, prio, dev, reps=5, warmup=2, flags=0, **knobs
 
 
 def table(rows):
-    cols = ["workload", "b_layout", "graph", "pace_all", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
+    cols = ["workload", "b_layout", "dep", "graph", "pace_all", "gemm_variant", "gemm_grid", "pad_kib", "comm_priority", "comm_wgs",
             "comm_rate_gbs", "gemm_wg_per_cu", "gemm_wg_per_cu_achieved", "t_seq_ms", "t_ovl_ms",
             "reduction_pct", "norm_time", "ideal_ovl_ms", "t_gemm_ms", "gemm_mfma_frac", "gemm_hbm_frac",
             "t_comm_ms", "comm_hbm_frac", "comm_ovl_us", "overlap_rate", "comm_coresident", "gemm_wg_us_alone",
@@ -124,9 +135,10 @@ def main(argv=None):
                     help="comma list of persistent GEMM grid caps to run each workload with "
                          "(0 = one workgroup per tile); the rows then show the engine clock "
                          "against the number of CUs the GEMM keeps busy")
-    ap.add_argument("--b-layout", default="nk", choices=["nk", "kn"],
-                    help="GEMM B stored N x K (occ_gemm) or K x N (occ_gemm_kn: the automatic "
-                         "variant only, so the pad and tile-size points are skipped)")
+    ap.add_argument("--b-layout", default="kn", choices=["kn", "nk"],
+                    help="GEMM B stored K x N (occ_gemm) or N x K (occ_gemm_bt)")
+    ap.add_argument("--dep", default="event", choices=["event", "counter"],
+                    help="per-iteration dependency of the overlapped schedule")
     ap.add_argument("--pace-all", action="store_true",
                     help="apply --rates to every schedule (OCC_RUN_PACE_ALL): emulates a collective "
                          "whose time is set by inter-GPU links")
@@ -135,21 +147,12 @@ def main(argv=None):
     rows = []
     for name in a.workloads.split(","):
         w = WORKLOADS[name]
-        A, B, C, comm = setup(w, dev)
-        if a.b_layout == "kn":
-            B = B.t().contiguous()  # the same op(B), stored K x N
-        # The pad sweep runs with the default tile (128 KiB of LDS: only small
-        # pads fit) and with tiles small enough for the pad to set residency:
-        # 128x256x32 (48 KiB, two per CU), 128x128x64 (96 KiB, three stages) and
-        # the paper's opt2 64x64x64.
-        if a.b_layout == "kn":
-            points = [dict(gemm_variant=0, gemm_grid=int(g)) for g in (a.gemm_grids or "0").split(",")]
-        elif name == "blocks":
-            # the paper's two tiles (opt1 64x64x32, opt2 64x64x64) over the
-            # thread-block counts of its tile-size study
-            points = [dict(gemm_variant=v, gemm_grid=x * x) for v in (6, 7) for x in BLOCK_COUNTS]
+        A, B, C, comm = setup(w, dev, a.b_layout)
+        if name == "blocks":
+            # the paper's two tiles over the thread-block counts of its tile-size study
+            points = [dict(gemm_variant=v, gemm_grid=x * x) for v in BLOCK_VARIANTS[a.b_layout] for x in BLOCK_COUNTS]
         elif name == "sweep":
-            points = [dict(gemm_variant=v) for v in (0, 25, 14, 7)]
+            points = [dict(gemm_variant=v) for v in SWEEP_VARIANTS[a.b_layout]]
         elif a.gemm_grids:
             points = [dict(gemm_variant=0, gemm_grid=int(g)) for g in a.gemm_grids.split(",")]
         else:
@@ -164,8 +167,9 @@ def main(argv=None):
                     for prio in prios:
                         fl = (occ.OCC_RUN_GRAPH if a.graph else 0) | (occ.OCC_RUN_PACE_ALL if a.pace_all else 0)
                         row = measure(w, A, B, C, comm, pad, prio, dev, flags=fl, b_layout=a.b_layout,
-                                      **knobs, **ex)
+                                      dep=a.dep, **knobs, **ex)
                         row["b_layout"] = a.b_layout
+                        row["dep"] = a.dep
                         row["graph"] = bool(a.graph)
                         row["pace_all"] = bool(a.pace_all)
                         row["comm_rate_gbs"] = ex["comm_rate_gbs"]
@@ -180,7 +184,7 @@ def main(argv=None):
                                                         tune_reps=3, b_layout=a.b_layout, **comm)
             row = {"workload": w.name + " (tuned)", "gemm_variant": "auto", "gemm_grid": knobs["gemm_grid"],
                    "pad_kib": knobs["lds_bytes"] >> 10, "comm_priority": knobs["comm_priority"],
-                   "comm_wgs": knobs["comm_wgs"], "t_seq_ms": round(r["t_seq_ms"], 4),
+                   "comm_wgs": knobs["comm_wgs"], "dep": knobs["dep"], "t_seq_ms": round(r["t_seq_ms"], 4),
                    "t_ovl_ms": round(r["t_ovl_ms"], 4), "reduction_pct": round(r["reduction_pct"], 2),
                    "t_gemm_ms": round(r["t_gemm_ms"], 4), "t_comm_ms": round(r["t_comm_ms"], 4),
                    "gemm_wg_per_cu": r["gemm_wg_per_cu"], "prefer_sequential": prefer_seq}

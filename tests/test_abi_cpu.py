@@ -55,49 +55,67 @@ def test_library_exports_every_declared_symbol(L):
 
 def test_strerror_and_version(L):
     from paper_2606_09200_amd import binding
-    for code in range(0, -7, -1):
+    for code in range(0, -8, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == binding.ABI_VERSION == (1, 4)
+    assert binding.occ_version() == binding.ABI_VERSION == (2, 0)
     hdr = open(HEADER).read()
-    assert "#define OCC_VERSION_MAJOR 1" in hdr and "#define OCC_VERSION_MINOR 4" in hdr
+    assert "#define OCC_VERSION_MAJOR 2" in hdr and "#define OCC_VERSION_MINOR 0" in hdr
 
 
 P = ctypes.c_void_p
 
 
 def test_gemm_argument_errors(L):
-    # bad sizes, K not a multiple of 8, null or misaligned pointers, aliasing
-    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), -1, 4, 8, 0, None) == -1
-    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), 4, 4, 12, 0, None) == -1
-    assert L.occ_gemm(None, P(0x2000), P(0x3000), 4, 4, 8, 0, None) == -1
-    assert L.occ_gemm(P(0x1008), P(0x2000), P(0x3000), 4, 4, 8, 0, None) == -1
-    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x1010), 4, 4, 8, 0, None) == -4  # C inside A
-    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, -1, 0, None) == -1
-    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, 0, -5, None) == -1
+    # occ_gemm takes B stored K x N: bad sizes, K or N not a multiple of 8,
+    # null or misaligned pointers, aliasing
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), -1, 8, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), 4, 8, 12, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None) == -1   # N % 8 (16-byte B rows)
+    assert L.occ_gemm(None, P(0x2000), P(0x3000), 4, 8, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), None, P(0x3000), 4, 8, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1008), P(0x2000), P(0x3000), 4, 8, 8, 0, None) == -1
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x1010), 4, 8, 8, 0, None) == -4     # C inside A
+    assert L.occ_gemm(P(0x1000), P(0x2000), P(0x2010), 4, 8, 8, 0, None) == -4     # C inside B
+    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, -1, 0, None) == -1
+    assert L.occ_gemm_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, 0, -5, None) == -1
 
 
-def test_gemm_kn_argument_errors(L):
-    # K x N B: 16-byte rows need N % 8 == 0, on top of occ_gemm's checks
-    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None) == -1
-    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x3000), 4, 8, 12, 0, None) == -1
-    assert L.occ_gemm_kn(P(0x1000), None, P(0x3000), 4, 8, 8, 0, None) == -1
-    assert L.occ_gemm_kn(P(0x1000), P(0x2000), P(0x2010), 4, 8, 8, 0, None) == -4  # C inside B
-    assert L.occ_gemm_kn_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, -1, 0, None) == -1
-    assert L.occ_gemm_kn_ex(P(0x1000), P(0x2000), P(0x3000), 4, 8, 8, 0, 0, -1, None) == -1
+def test_gemm_bt_argument_errors(L):
+    # occ_gemm_bt takes B stored N x K: the same checks except N % 8
+    assert L.occ_gemm_bt(P(0x1000), P(0x2000), P(0x3000), 4, 4, 12, 0, None) == -1
+    assert L.occ_gemm_bt(None, P(0x2000), P(0x3000), 4, 4, 8, 0, None) == -1
+    assert L.occ_gemm_bt(P(0x1000), P(0x2000), P(0x1010), 4, 4, 8, 0, None) == -4  # C inside A
+    assert L.occ_gemm_bt_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, -1, 0, None) == -1
+    assert L.occ_gemm_bt_ex(P(0x1000), P(0x2000), P(0x3000), 4, 4, 8, 0, 0, -1, None) == -1
     # N % 8 != 0 is fine for the N x K layout (fails later, with no device)
-    expect_accepted(L, L.occ_gemm, P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None)
+    expect_accepted(L, L.occ_gemm_bt, P(0x1000), P(0x2000), P(0x3000), 4, 12, 8, 0, None)
 
 
-def test_gemm_kn_plan_query_argument_errors(L):
+def test_gemm_plan_query_argument_errors(L):
     from paper_2606_09200_amd import binding
     plan = binding.occ_gemm_plan()
-    assert L.occ_gemm_kn_plan_query(16, 64, 64, 0, 0, 0, None) == -1
-    assert L.occ_gemm_kn_plan_query(-1, 64, 64, 0, 0, 0, ctypes.byref(plan)) == -1
-    assert L.occ_gemm_kn_plan_query(16, 64, 64, 0, -1, 0, ctypes.byref(plan)) == -1
-    assert L.occ_gemm_kn_plan_query(16, 64, 64, 0, 0, -1, ctypes.byref(plan)) == -1
+    for q in (L.occ_gemm_plan_query, L.occ_gemm_bt_plan_query):
+        assert q(16, 64, 64, 0, 0, 0, None) == -1
+        assert q(-1, 64, 64, 0, 0, 0, ctypes.byref(plan)) == -1
+        assert q(16, 64, 64, 0, -1, 0, ctypes.byref(plan)) == -1
+        assert q(16, 64, 64, 0, 0, -1, ctypes.byref(plan)) == -1
     with pytest.raises(ValueError):
         binding.occ_gemm_plan_query(16, 64, 64, b_layout="nn")
+
+
+def test_binding_variant_tables_match_header():
+    """Every variant id the header names is in the binding's table of its
+    layout, and nothing else is."""
+    from paper_2606_09200_amd import binding
+    text = open(HEADER).read()
+    enum = text[text.index("OCC_GEMM_AUTO = 0"):]
+    enum = enum[:enum.index("};")]
+    kn = {int(v) for v in re.findall(r"OCC_GEMM_KN_\w+ = (\d+)", enum)}
+    ids = {int(v) for v in re.findall(r"OCC_GEMM_\w+ = (\d+)", enum)} - {0}
+    assert kn == set(binding.KN_VARIANTS)
+    assert ids - kn == set(binding.NK_VARIANTS)
+    assert set(binding.SKINNY_VARIANTS) <= ids
 
 
 def test_reduce_argument_errors(L):
@@ -178,9 +196,18 @@ def test_run_overlap_argument_errors(L):
     cfg.flags = 16                                                        # OCC_RUN_PACE_ALL is valid
     expect_accepted(L, L.run_overlap, ctypes.byref(cfg), ctypes.byref(res))
     cfg.flags = 0
-    cfg.gemm_b_layout = 2                                                 # neither N x K nor K x N
+    cfg.gemm_b_layout = 2                                                 # neither K x N nor N x K
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
     cfg.gemm_b_layout = 0
+    cfg.dep = 2                                                           # neither event nor counter
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.dep, cfg.n_iter = 1, 1025                                         # counters for 1024 iterations
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.n_iter = 2
+    expect_accepted(L, L.run_overlap, ctypes.byref(cfg), ctypes.byref(res))
+    cfg.flags = 8 | 2                                                     # graphs keep the event
+    assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
+    cfg.flags, cfg.dep = 0, 0
     cfg.comm_kind, cfg.len = 2, 32                                        # own reduce: len must be M*N
     cfg.out = 0x40000
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
@@ -191,11 +218,11 @@ def test_run_overlap_argument_errors(L):
     cfg.M, cfg.N, cfg.len, cfg.out = 3, 3, 9, 0x40000                     # M*N not a multiple of 8
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
     cfg.M, cfg.N, cfg.len, cfg.comm_kind, cfg.out = 8, 8, 64, 0, 0x30000
-    cfg.gemm_b_layout, cfg.N = 1, 12                                      # K x N needs N % 8 == 0
+    cfg.N = 12                                                            # K x N needs N % 8 == 0
     assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1
-    cfg.N = 8
+    cfg.gemm_b_layout = 1                                                 # N x K does not
     expect_accepted(L, L.run_overlap, ctypes.byref(cfg), ctypes.byref(res))
-    cfg.gemm_b_layout = 0
+    cfg.gemm_b_layout, cfg.N = 0, 8
     for rate in (-1.0, 5.0, float("nan"), 1e7):                          # pacing out of range
         cfg.comm_rate_gbs = rate
         assert L.run_overlap(ctypes.byref(cfg), ctypes.byref(res)) == -1, rate

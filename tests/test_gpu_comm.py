@@ -161,7 +161,8 @@ def test_reduce_empty_is_noop():
     assert torch.all(out == 7.0)
 
 
-@pytest.mark.parametrize("name", ["tiny", "mb", "cb"])
+# paper_cb_ar: Table 1's 896 MiB allreduce share, 4 chunks of 224 MiB
+@pytest.mark.parametrize("name", ["tiny", "mb", "cb", "paper_cb_ar"])
 def test_reduce_workload_sizes_bit_exact(name):
     from paper_2606_09200_amd.workloads import WORKLOADS
     w = WORKLOADS[name]
@@ -222,9 +223,11 @@ def test_permute_knobs_do_not_change_bits(wgs, priority):
     assert np.array_equal(gpu_permute(src, perm, 1 << 16, wgs=wgs, priority=priority), want)
 
 
-def test_permute_workload_size_bit_exact():
+# paper_cb_a2a: Table 1's 896 MiB alltoall share, 4 chunks of 224 MiB
+@pytest.mark.parametrize("name", ["a2a", "paper_cb_a2a"])
+def test_permute_workload_size_bit_exact(name):
     from paper_2606_09200_amd.workloads import WORKLOADS
-    w = WORKLOADS["a2a"]
+    w = WORKLOADS[name]
     src = inputs.permute_payload(w.nchunks, w.chunk_bytes, seed=2, device=DEV)
     perm = inputs.chunk_permutation(w.nchunks, seed=3)
     dst = torch.empty_like(src)
