@@ -8,8 +8,10 @@ input generators, which hold none of the method's arithmetic.
 What each function computes (the plain definitions, see ``oracle.c``):
 
 * :func:`gemm_bf16` -- Background, item 1 (the GEMM ``C = alpha op(A) op(B) +
-  beta C``), read with alpha = 1, beta = 0: exact-product binary64 sums, one
-  round-to-nearest-even to bfloat16.
+  beta C``), read with alpha = 1, beta = 0: the products accumulated in
+  binary32 in increasing k (``acc="f32"``, the workload's definition) or
+  summed exactly in binary64 (``acc="f64"``), then one round-to-nearest-even
+  to bfloat16.
 * :func:`chunk_sum_f32` -- Background, item 2 (allreduce aggregates local
   gradients): one GPU's share is the element-wise binary32 sum of its chunks
   in the fixed order ``c0 + c1 + ... + c_{n-1}``.
@@ -36,6 +38,8 @@ def _load():
             ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
             ctypes.c_void_p]
         lib.oracle_gemm_bf16_block.restype = None
+        lib.oracle_gemm_bf16_f32acc_block.argtypes = lib.oracle_gemm_bf16_block.argtypes
+        lib.oracle_gemm_bf16_f32acc_block.restype = None
         lib.oracle_chunk_sum_f32.argtypes = [
             ctypes.POINTER(ctypes.c_void_p), ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p]
         lib.oracle_chunk_sum_f32.restype = None
@@ -83,13 +87,14 @@ def bf16_to_double(h: int) -> float:
     return float(_load().oracle_bf16_to_double(int(h) & 0xFFFF))
 
 
-def gemm_bf16(A, B, M, N, K, b_layout="nk", rows=None, cols=None):
+def gemm_bf16(A, B, M, N, K, b_layout="nk", rows=None, cols=None, acc="f32"):
     """bf16 bit patterns of ``C = A @ op(B)``, or of its block ``C[rows, cols]``.
 
     ``A`` is M x K row-major.  ``b_layout="nk"``: ``B`` is stored N x K (a linear
     layer's weight, op(B) = B^T); ``"kn"``: ``B`` is stored K x N.
     ``rows``/``cols`` are half-open ``(start, stop)`` ranges (default: all).
-    Returns a numpy uint16 array of shape (rows, cols).
+    ``acc="f32"``: binary32 accumulation in increasing k; ``"f64"``: the exact
+    sum.  Returns a numpy uint16 array of shape (rows, cols).
     """
     a = _u16(A).reshape(-1)
     b = _u16(B).reshape(-1)
@@ -101,8 +106,8 @@ def gemm_bf16(A, B, M, N, K, b_layout="nk", rows=None, cols=None):
         raise ValueError("block out of range")
     out = np.empty((m1 - m0, n1 - n0), dtype=np.uint16)
     lay = {"nk": 0, "kn": 1}[b_layout]
-    _load().oracle_gemm_bf16_block(a.ctypes.data, b.ctypes.data, M, N, K, lay,
-                                   m0, m1, n0, n1, out.ctypes.data)
+    fn = {"f32": _load().oracle_gemm_bf16_f32acc_block, "f64": _load().oracle_gemm_bf16_block}[acc]
+    fn(a.ctypes.data, b.ctypes.data, M, N, K, lay, m0, m1, n0, n1, out.ctypes.data)
     return out
 
 

@@ -10,9 +10,13 @@
  * for a reader to check by eye, with no blocking, fusion or reordering:
  *
  *   - GEMM (Background, item 1: C = alpha*op(A)*op(B) + beta*C, read here
- *     with alpha = 1, beta = 0): every output is the sum over k of the
- *     products, accumulated in binary64 (each bf16*bf16 product is exact in
- *     binary64), then rounded once to bfloat16, round-to-nearest-even.
+ *     with alpha = 1, beta = 0), two definitions: (a) the workload's, the
+ *     products accumulated in binary32 in increasing k (each bf16*bf16
+ *     product is exact in binary32: 8-bit significands), then rounded once
+ *     to bfloat16; (b) the sum accumulated in binary64 (each product exact,
+ *     the sum's rounding error far below one bfloat16 step at these
+ *     magnitudes: a stand-in for the exact sum), then rounded once to
+ *     bfloat16.  Both round to nearest, ties to even.
  *   - Local share of an allreduce (Background, item 2: local gradients are
  *     aggregated across GPUs): element-wise sum of the chunks in binary32,
  *     strict left-to-right order c0 + c1 + ... + c_{n-1}.  The fixed order
@@ -98,6 +102,32 @@ void oracle_gemm_bf16_block(const uint16_t *A, const uint16_t *B, int M, int N, 
         acc += a * b;
       }
       out[(size_t)(m - m0) * ncols + (n - n0)] = oracle_double_to_bf16(acc);
+    }
+  }
+}
+
+/*
+ * The same block with the products accumulated in binary32, one addition per
+ * k in increasing order (acc = acc + a*b, no fused multiply-add: the build
+ * forbids contraction), then rounded once to bfloat16 through binary64 (the
+ * widening is exact).
+ */
+void oracle_gemm_bf16_f32acc_block(const uint16_t *A, const uint16_t *B, int M, int N, int K,
+                                   int b_layout, int m0, int m1, int n0, int n1, uint16_t *out) {
+  (void)M;
+  int ncols = n1 - n0;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int m = m0; m < m1; ++m) {
+    for (int n = n0; n < n1; ++n) {
+      float acc = 0.0f;
+      for (int k = 0; k < K; ++k) {
+        float a = (float)oracle_bf16_to_double(A[(size_t)m * K + k]);
+        float b = b_layout == 0 ? (float)oracle_bf16_to_double(B[(size_t)n * K + k])
+                                : (float)oracle_bf16_to_double(B[(size_t)k * N + n]);
+        float p = a * b;
+        acc = acc + p;
+      }
+      out[(size_t)(m - m0) * ncols + (n - n0)] = oracle_double_to_bf16((double)acc);
     }
   }
 }

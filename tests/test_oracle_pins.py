@@ -4,11 +4,18 @@ Each check is chosen so that a plausible slip in the oracle -- a transposed
 operand, a dropped term, a wrong index, a reassociated sum, double rounding,
 a wrong tie rule -- fails at least one of them:
 
-* GEMM: exact rational brute force (fractions.Fraction) followed by an
-  independent round-to-nearest-even written here; integer-valued operands
-  whose sums are exact, checked against numpy's int64 matmul and torch's
-  float32 -> bfloat16 conversion; identity and all-ones closed forms;
-  a float64 BLAS cross-check within one bfloat16 ulp; both B layouts.
+* GEMM, binary64 sum (acc="f64"): exact rational brute force
+  (fractions.Fraction) followed by an independent round-to-nearest-even
+  written here; a float64 BLAS cross-check within one bfloat16 ulp.
+* GEMM, binary32 accumulation in increasing k (acc="f32", the default):
+  hand-derived order probes (tests/golden/gemm_f32acc_order.txt) whose
+  result differs from the exact sum and from the reversed order; within
+  K * 2^-24 * sum |a b| of the exact sum (plus the final rounding) on random
+  operands.
+* Both: integer-valued operands whose sums are exact, checked against
+  numpy's int64 matmul and torch's float32 -> bfloat16 conversion; identity
+  and all-ones closed forms; both B layouts; blocks are slices of the full
+  result.
 * bfloat16 rounding: a hand-derived table (tests/golden/bf16_rne.txt).
 * Chunk sum: order probes whose left-fold result differs from any other
   order (tests/golden/chunk_sum_order.txt); all-ones -> nchunks; integer
@@ -135,13 +142,42 @@ def test_bf16_roundtrip_all_finite_patterns():
 def test_gemm_exact_rational(M, N, K, seed):
     A = random_bf16((M, K), seed)
     B = random_bf16((N, K), seed + 100)
-    got = oracle.gemm_bf16(A, B, M, N, K)
+    got = oracle.gemm_bf16(A, B, M, N, K, acc="f64")
     a = A.view(torch.int16).numpy().view(np.uint16)
     b = B.view(torch.int16).numpy().view(np.uint16)
     for m in range(M):
         for n in range(N):
             exact = sum(bf16_value(a[m, k]) * bf16_value(b[n, k]) for k in range(K))
             assert got[m, n] == rne_bf16_exact(exact), (m, n)
+
+
+@pytest.mark.parametrize("row", _golden_rows("gemm_f32acc_order.txt"), ids=lambda r: r[0])
+def test_gemm_accumulation_order_probes(row):
+    a = [eval(v) for v in row[0].split(",")]
+    b = [eval(v) for v in row[1].split(",")]
+    K = len(a)
+    A = torch.tensor([a], dtype=torch.float32).to(torch.bfloat16)
+    B = torch.tensor([b], dtype=torch.float32).to(torch.bfloat16)      # N x K, N = 1
+    assert A.float().tolist()[0] == a and B.float().tolist()[0] == b   # the values are bf16
+    assert oracle.gemm_bf16(A, B, 1, 1, K, acc="f32")[0, 0] == int(row[2], 16)
+    assert oracle.gemm_bf16(A, B, 1, 1, K, acc="f64")[0, 0] == int(row[3], 16)
+    # the same with B stored K x N
+    assert oracle.gemm_bf16(A, B.t().contiguous(), 1, 1, K, b_layout="kn")[0, 0] == int(row[2], 16)
+
+
+@pytest.mark.parametrize("M,N,K,seed", [(16, 24, 512, 5), (9, 40, 2048, 6)])
+def test_gemm_f32_accumulation_within_bound_of_exact(M, N, K, seed):
+    A = random_bf16((M, K), seed)
+    B = random_bf16((N, K), seed + 1)
+    got = bf16_bits_to_f64(oracle.gemm_bf16(A, B, M, N, K, acc="f32"))
+    a, b = A.double().numpy(), B.double().numpy()
+    exact = a @ b.T                          # float64 BLAS: error far below the bound
+    bound = K * 2.0 ** -24 * (np.abs(a) @ np.abs(b).T)
+    half_ulp = np.maximum(np.abs(exact) + bound, 2.0 ** -126) * 2.0 ** -8
+    assert np.all(np.abs(got - exact) <= bound + half_ulp)
+    # and the two definitions agree on most outputs
+    same = oracle.gemm_bf16(A, B, M, N, K, acc="f32") == oracle.gemm_bf16(A, B, M, N, K, acc="f64")
+    assert same.mean() > 0.95
 
 
 @pytest.mark.parametrize("M,N,K", [(37, 29, 512), (64, 8, 136), (7, 130, 256)])
@@ -153,7 +189,8 @@ def test_gemm_integer_operands_exact(M, N, K):
     B = torch.from_numpy(bi.astype(np.float32)).to(torch.bfloat16)
     exact = ai @ bi.T                               # int64 library matmul
     want = to_bf16_bits_torch(exact.astype(np.float32))  # |sum| < 2^24: float32 is exact
-    assert np.array_equal(oracle.gemm_bf16(A, B, M, N, K), want)
+    assert np.array_equal(oracle.gemm_bf16(A, B, M, N, K, acc="f32"), want)
+    assert np.array_equal(oracle.gemm_bf16(A, B, M, N, K, acc="f64"), want)
 
 
 def test_gemm_identity_and_ones():
@@ -177,9 +214,11 @@ def test_gemm_layouts_agree_and_blas_within_one_ulp():
     A = random_bf16((M, K), 21)
     Bnk = random_bf16((N, K), 22)
     Bkn = Bnk.t().contiguous()
-    c_nk = oracle.gemm_bf16(A, Bnk, M, N, K, b_layout="nk")
-    c_kn = oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn")
+    c_nk = oracle.gemm_bf16(A, Bnk, M, N, K, b_layout="nk", acc="f64")
+    c_kn = oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn", acc="f64")
     assert np.array_equal(c_nk, c_kn)
+    assert np.array_equal(oracle.gemm_bf16(A, Bnk, M, N, K, b_layout="nk"),
+                          oracle.gemm_bf16(A, Bkn, M, N, K, b_layout="kn"))
     ref = A.double().numpy() @ Bnk.double().numpy().T    # float64 BLAS
     got = bf16_bits_to_f64(c_nk)
     ulp = np.maximum(np.abs(ref), 2.0 ** -126) * 2.0 ** -7
