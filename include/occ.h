@@ -402,6 +402,44 @@ int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res);
 int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                      int *prefer_sequential);
 
+/*
+ * occ_overlap_workspace_bytes -- device bytes occ_overlap_enqueue needs for
+ * n_iter iterations: 2 * n_iter + 1 uint32 counters, rounded up to 256
+ * bytes (0 for n_iter < 1).
+ */
+size_t occ_overlap_workspace_bytes(int n_iter);
+
+/*
+ * occ_overlap_enqueue -- enqueue the overlapped schedule of *cfg and return
+ * (Section 3.2, Fig. 1b): for i < n_iter, K_g^i on cfg->stream and K_c^i on
+ * comm_stream, with K_g^i -> K_c^i kept by the device counter of
+ * OCC_DEP_COUNTER in `workspace`.  No timing, no runtime events, no host
+ * synchronisation and no allocation: the form a training or serving loop
+ * calls.  GEMM and collective as in run_overlap (gemm_b_layout,
+ * comm_kind, knobs, comm_rate_gbs pacing every collective); reps, warmup,
+ * flags and dep are not read; timeline and wg_trace must be NULL.
+ *   workspace : caller-owned device buffer of at least
+ *               occ_overlap_workspace_bytes(n_iter) bytes, 4-byte aligned,
+ *               all zero before its first use.  A schedule leaves it zero
+ *               again once all its collectives have passed their waits.
+ *   err       : optional device uint32 (may be NULL) that a collective
+ *               workgroup sets to 1 when its bounded wait runs out (the
+ *               library never clears it).
+ * Ordering is the caller's: both streams must already follow the work that
+ * produces the inputs; the collectives' outputs are complete when
+ * comm_stream reaches the end of this call's work, C when cfg->stream does.
+ * Two schedules on one workspace must not overlap: order the next call's
+ * cfg->stream after this call's comm_stream (else a GEMM can count into a
+ * counter a collective of this call still has to clear, and its own
+ * collective then waits out its bound).  Under stream capture the replay
+ * must run the two streams' chains concurrently, as captured.
+ * Errors: those of run_overlap, and OCC_EINVAL for a NULL, misaligned or
+ * short workspace, a comm grid above one workgroup per CU, or a collective
+ * with no work.
+ */
+int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
+                        uint32_t *err);
+
 /* Static string naming a status code. */
 const char *occ_strerror(int status);
 
@@ -409,7 +447,7 @@ const char *occ_strerror(int status);
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
 #define OCC_VERSION_MAJOR 2
-#define OCC_VERSION_MINOR 0
+#define OCC_VERSION_MINOR 1
 int occ_version(void);
 
 #ifdef __cplusplus

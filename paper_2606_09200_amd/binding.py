@@ -34,7 +34,7 @@ NK_VARIANTS = {
     25: "dl+pipe 128x256x32 4w 2st 2wg/cu", 34: "skinny M<=16, A in registers, B through LDS (K%1024==0, K<=8192)",
 }
 SKINNY_VARIANTS = (21, 33, 34)     # M <= 16 only
-ABI_VERSION = (2, 0)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+ABI_VERSION = (2, 1)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -101,6 +101,8 @@ _SIGS = {
     "run_overlap": [ctypes.POINTER(occ_overlap_cfg), ctypes.POINTER(occ_overlap_result)],
     "occ_overlap_tune": [ctypes.POINTER(occ_overlap_cfg), ctypes.c_int,
                          ctypes.POINTER(occ_overlap_result), ctypes.POINTER(ctypes.c_int)],
+    "occ_overlap_workspace_bytes": [ctypes.c_int],
+    "occ_overlap_enqueue": [ctypes.POINTER(occ_overlap_cfg), _P, _P, ctypes.c_size_t, _P],
     "occ_strerror": [ctypes.c_int],
     "occ_version": [],
 }
@@ -117,7 +119,8 @@ def lib():
         for name, args in _SIGS.items():
             f = getattr(L, name)
             f.argtypes = args
-            f.restype = ctypes.c_char_p if name == "occ_strerror" else ctypes.c_int
+            f.restype = (ctypes.c_char_p if name == "occ_strerror" else
+                         ctypes.c_size_t if name == "occ_overlap_workspace_bytes" else ctypes.c_int)
         v = L.occ_version()
         if (v >> 16, v & 0xFFFF) != ABI_VERSION:
             raise RuntimeError("%s has ABI version %d.%d, this binding expects %d.%d; rebuild it with "
@@ -419,3 +422,29 @@ def occ_overlap_tune(A, B, C, *, bufs=None, out=None, src=None, dst=None, perm=N
              "gemm_grid": cfg.gemm_grid, "lds_bytes": cfg.lds_bytes,
              "dep": "counter" if cfg.dep == OCC_DEP_COUNTER else "event"}
     return knobs, {f: getattr(res, f) for f, _ in occ_overlap_result._fields_}, bool(pref.value)
+
+
+def occ_overlap_workspace_bytes(n_iter):
+    """Device bytes occ_overlap_enqueue needs for n_iter iterations."""
+    return int(lib().occ_overlap_workspace_bytes(int(n_iter)))
+
+
+def occ_overlap_enqueue(A, B, C, *, workspace, comm_stream, err=None, bufs=None, out=None, src=None, dst=None,
+                        perm=None, chunk_bytes=0, lds_bytes=0, gemm_variant=0, gemm_grid=0, gemm_priority=0,
+                        comm_wgs=0, comm_priority=0, n_iter=10, comm_rate_gbs=0.0, b_layout="kn",
+                        reduce_own=False, stream=None):
+    """Enqueue the overlapped schedule (GEMMs on ``stream``, default torch's
+    current stream; collectives on ``comm_stream``) with the device-counter
+    dependency in ``workspace`` (a zeroed GPU tensor of at least
+    occ_overlap_workspace_bytes(n_iter) bytes) and return; ``err``: optional
+    int32 GPU tensor of one element set to 1 if a bounded wait ran out."""
+    cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
+                          gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, 1, 0, 0, None, None,
+                          comm_rate_gbs, b_layout, reduce_own, "counter", stream)
+    if not workspace.is_cuda or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous GPU tensor")
+    if err is not None and (not err.is_cuda or err.element_size() != 4 or err.numel() < 1):
+        raise ValueError("err must be a 32-bit GPU tensor")
+    _check(lib().occ_overlap_enqueue(ctypes.byref(cfg), _stream(comm_stream), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(), _ptr(err)),
+           "occ_overlap_enqueue")

@@ -100,6 +100,9 @@ int current_device_info(const DeviceInfo **out) {
 }
 
 int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res);
+size_t overlap_workspace_bytes(int n_iter);
+int overlap_enqueue_impl(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
+                         uint32_t *err);
 int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                       int *prefer_sequential);
 
@@ -217,6 +220,13 @@ int run_overlap(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
 int occ_overlap_tune(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                      int *prefer_sequential) {
   return occ::overlap_tune_impl(cfg, tune_reps, res, prefer_sequential);
+}
+
+size_t occ_overlap_workspace_bytes(int n_iter) { return occ::overlap_workspace_bytes(n_iter); }
+
+int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
+                        uint32_t *err) {
+  return occ::overlap_enqueue_impl(cfg, comm_stream, workspace, workspace_bytes, err);
 }
 
 const char *occ_strerror(int status) {

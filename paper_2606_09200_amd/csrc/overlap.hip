@@ -250,6 +250,42 @@ struct Graph {
 
 }  // namespace
 
+void make_launcher(const occ_overlap_cfg &c, Launcher *L) {
+  const KHooks off{};
+  L->kind = c.comm_kind;
+  L->g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
+                  c.gemm_priority, off, c.gemm_b_layout == OCC_B_KN};
+  L->r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
+  L->own = c.comm_kind == OCC_COMM_REDUCE_OWN;
+  if (L->own) L->r.own = static_cast<const uint16_t *>(c.C);
+  L->p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
+  L->rate_gbs = c.comm_rate_gbs;
+  L->pace_all = (c.flags & OCC_RUN_PACE_ALL) != 0;
+}
+
+// Workgroups of one collective launch.
+int comm_grid(const occ_overlap_cfg &c, const Launcher &L) {
+  return c.comm_wgs > 0 ? c.comm_wgs
+                        : (c.comm_kind != OCC_COMM_PERMUTE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
+}
+
+// Per-iteration hooks of the counter dependency over `n` iterations with
+// counters tk[0..n) (GEMM workgroups done) and ack[0..n) (collective
+// workgroups past their wait), timeouts reported in *err.
+void counter_hooks(const Launcher &L, int n, uint32_t gemm_grid, uint32_t *tk, uint32_t *ack, uint32_t *err,
+                   std::vector<KHooks> *hg, std::vector<KHooks> *hc) {
+  const uint32_t target = (L.g.M > 0 && L.g.N > 0) ? gemm_grid : 0u;
+  for (int i = 0; i < n; ++i) {
+    (*hg)[i].signal = tk + i;
+    (*hg)[i].release = L.own ? 1u : 0u;
+    (*hc)[i].wait = tk + i;
+    (*hc)[i].ack = ack + i;
+    (*hc)[i].err = err;
+    (*hc)[i].wait_target = target;
+    (*hc)[i].acquire = L.own ? 1u : 0u;
+  }
+}
+
 int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   if (res == nullptr) return OCC_EINVAL;
   OCC_TRY(validate_cfg(cfg));
@@ -262,24 +298,15 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   const int n = c.n_iter;
 
   Launcher L;
-  L.kind = c.comm_kind;
+  make_launcher(c, &L);
   const KHooks off{};
-  L.g = GemmCall{c.A, c.B, c.C, c.M, c.N, c.K, c.lds_bytes, c.gemm_grid, c.gemm_variant,
-                 c.gemm_priority, off, c.gemm_b_layout == OCC_B_KN};
-  L.r = ReduceCall{c.bufs, c.nchunks, c.len, c.out, c.comm_wgs, c.comm_priority, off, 0.0};
-  L.own = c.comm_kind == OCC_COMM_REDUCE_OWN;
-  if (L.own) L.r.own = static_cast<const uint16_t *>(c.C);
-  L.p = PermuteCall{c.src, c.dst, c.perm, c.nchunks, c.chunk_bytes, c.comm_wgs, c.comm_priority, off, 0.0};
-  L.rate_gbs = c.comm_rate_gbs;
-  L.pace_all = (c.flags & OCC_RUN_PACE_ALL) != 0;
 
   occ_gemm_plan plan;
   OCC_TRY(gemm_plan(L.g, &plan));
   res->gemm_wg_per_cu = plan.wg_per_cu;
   res->gemm_grid = plan.grid;
   res->gemm_tile_lds = plan.tile_lds_bytes;
-  res->comm_wgs = c.comm_wgs > 0 ? c.comm_wgs
-                  : (c.comm_kind != OCC_COMM_PERMUTE ? reduce_default_wgs(L.r) : permute_default_wgs(L.p));
+  res->comm_wgs = comm_grid(c, L);
 
   // The counter dependency: every collective workgroup may wait on a CU
   // beside the GEMM, so at most one per CU (then some CU always has room for
@@ -318,16 +345,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
   // only when the collective reads the GEMM's output.
   std::vector<KHooks> hg(n, off), hc(n, off);
   if (counter) {
-    const uint32_t target = (c.M > 0 && c.N > 0) ? (uint32_t)plan.grid : 0u;
-    for (int i = 0; i < n; ++i) {
-      hg[i].signal = dep + i;
-      hg[i].release = L.own ? 1u : 0u;
-      hc[i].wait = dep + i;
-      hc[i].ack = dep + kMaxDepIter + i;
-      hc[i].err = dep + 2 * kMaxDepIter;
-      hc[i].wait_target = target;
-      hc[i].acquire = L.own ? 1u : 0u;
-    }
+    counter_hooks(L, n, (uint32_t)plan.grid, dep, dep + kMaxDepIter, dep + 2 * kMaxDepIter, &hg, &hc);
     // every counter at zero (a call that failed half-way may have left some)
     OCC_HIP(hipMemsetAsync(dep, 0, kDepWords * sizeof(uint32_t), s0));
   }
@@ -548,6 +566,57 @@ int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *r
   OCC_TRY(run_overlap_impl(cfg, res));
   *prefer_sequential = (res->t_seq_median_ms > 0 && res->t_ovl_median_ms > res->t_seq_median_ms) ? 1 : 0;
   return OCC_OK;
+}
+
+// The overlapped schedule enqueued without timing or runtime events: GEMMs on
+// s0, collectives on s1, K_g^i -> K_c^i by the device counters tk/ack (n
+// each, zero on entry, zero again once every collective has passed its
+// wait).
+int enqueue_impl(const occ_overlap_cfg *cfg, hipStream_t s1, uint32_t *tk, uint32_t *ack, int capacity,
+                 uint32_t *err, uint32_t *err_sink) {
+  if (cfg == nullptr) return OCC_EINVAL;
+  occ_overlap_cfg c = *cfg;
+  // the fields a timed run uses are not read here
+  c.reps = 1;
+  c.warmup = 0;
+  c.flags = OCC_RUN_OVL;
+  c.dep = OCC_DEP_COUNTER;
+  if (cfg->timeline != nullptr || cfg->wg_trace != nullptr) return OCC_EINVAL;
+  OCC_TRY(validate_cfg(&c));
+  if (c.n_iter > capacity) return OCC_EINVAL;
+  if ((c.comm_kind == OCC_COMM_PERMUTE ? c.chunk_bytes : c.len) == 0) return OCC_EINVAL;
+  const DeviceInfo *di = nullptr;
+  OCC_TRY(current_device_info(&di));
+  Launcher L;
+  make_launcher(c, &L);
+  if (comm_grid(c, L) > di->num_cus) return OCC_EINVAL;
+  occ_gemm_plan plan;
+  OCC_TRY(gemm_plan(L.g, &plan));
+  const int n = c.n_iter;
+  std::vector<KHooks> hg(n), hc(n);
+  counter_hooks(L, n, (uint32_t)plan.grid, tk, ack, err != nullptr ? err : err_sink, &hg, &hc);
+  hipStream_t s0 = static_cast<hipStream_t>(c.stream);
+  for (int i = 0; i < n; ++i) {
+    OCC_TRY(L.gemm(s0, hg[i], i));
+    OCC_TRY(L.comm(s1, hc[i], true, i));
+  }
+  return OCC_OK;
+}
+
+size_t overlap_workspace_bytes(int n_iter) {
+  if (n_iter < 1) return 0;
+  const size_t words = 2 * (size_t)n_iter + 1;
+  return (words * sizeof(uint32_t) + 255) & ~(size_t)255;
+}
+
+int overlap_enqueue_impl(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
+                         uint32_t *err) {
+  if (cfg == nullptr || workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 3u) != 0)
+    return OCC_EINVAL;
+  if (cfg->n_iter < 1 || workspace_bytes < overlap_workspace_bytes(cfg->n_iter)) return OCC_EINVAL;
+  uint32_t *w = static_cast<uint32_t *>(workspace);
+  const int n = cfg->n_iter;
+  return enqueue_impl(cfg, static_cast<hipStream_t>(comm_stream), w, w + n, n, err, w + 2 * n);
 }
 
 }  // namespace occ

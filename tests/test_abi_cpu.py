@@ -58,9 +58,9 @@ def test_strerror_and_version(L):
     for code in range(0, -8, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == binding.ABI_VERSION == (2, 0)
+    assert binding.occ_version() == binding.ABI_VERSION == (2, 1)
     hdr = open(HEADER).read()
-    assert "#define OCC_VERSION_MAJOR 2" in hdr and "#define OCC_VERSION_MINOR 0" in hdr
+    assert "#define OCC_VERSION_MAJOR 2" in hdr and "#define OCC_VERSION_MINOR 1" in hdr
 
 
 P = ctypes.c_void_p
@@ -250,3 +250,32 @@ def test_overlap_tune_argument_errors(L):
     assert L.occ_overlap_tune(ctypes.byref(cfg), 2, ctypes.byref(res), None) == -1
     cfg.n_iter = 0  # invalid schedule: rejected before any device call
     assert L.occ_overlap_tune(ctypes.byref(cfg), 2, ctypes.byref(res), ctypes.byref(pref)) == -1
+
+
+def test_overlap_enqueue_argument_errors(L):
+    from paper_2606_09200_amd import binding as b
+    assert L.occ_overlap_workspace_bytes(0) == 0
+    assert L.occ_overlap_workspace_bytes(1) == 256
+    assert L.occ_overlap_workspace_bytes(10) == 256
+    assert L.occ_overlap_workspace_bytes(100) == 1024      # 201 words, rounded up to 256 bytes
+    cfg = b.occ_overlap_cfg()
+    cfg.M = cfg.N = cfg.K = 8
+    cfg.A, cfg.B, cfg.C = 0x1000, 0x2000, 0x3000
+    arr = (ctypes.c_void_p * 2)(0x10000, 0x20000)
+    cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    cfg.nchunks, cfg.len, cfg.out, cfg.n_iter = 2, 64, 0x30000, 4
+    ws = P(0x50000)
+    assert L.occ_overlap_enqueue(None, None, ws, 256, None) == -1
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, None, 256, None) == -1     # no workspace
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, P(0x50002), 256, None) == -1  # misaligned
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, ws, 16, None) == -1       # too short
+    cfg.timeline = 0x60000                                                         # no tracing here
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, ws, 256, None) == -1
+    cfg.timeline = None
+    cfg.out = 0x3000 + 16                                                          # output inside C
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, ws, 256, None) == -4
+    cfg.out = 0x30000
+    cfg.reps, cfg.warmup, cfg.flags, cfg.dep = 0, -1, 8, 0                        # fields it does not read
+    expect_accepted(L, L.occ_overlap_enqueue, ctypes.byref(cfg), None, ws, 256, None)
+    cfg.n_iter = 0
+    assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, ws, 256, None) == -1

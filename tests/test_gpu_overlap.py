@@ -451,3 +451,69 @@ def test_overlap_reduce_own_no_peers_and_timeline(dep):
                           C[-1].view(torch.int16).cpu().numpy().view(np.uint16).reshape(-1).astype(np.uint32) << 16)
     g, c = timeline_intervals(tl, n_iter)
     assert schedule.dependency_violations(g, c) == []
+
+
+# ------------------------------------------------------- occ_overlap_enqueue
+@pytest.mark.parametrize("kind", ["reduce", "permute", "own"])
+def test_overlap_enqueue_matches_plain_calls(kind):
+    """The enqueued overlapped schedule (no events, device counters in a
+    caller workspace) computes what the plain calls compute, reports no
+    timeout, and leaves its workspace zeroed for the next schedule, which
+    runs on the same workspace with fewer iterations."""
+    M, N, K = 520, 264, 136
+    A, Bt = inputs.gemm_operands(M, N, K, seed=3, device=DEV)
+    B = Bt.t().contiguous()
+    s1 = torch.cuda.Stream()
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for n_iter in (6, 3):
+        nbytes = occ.occ_overlap_workspace_bytes(n_iter)
+        ws = torch.zeros(nbytes // 4, dtype=torch.int32, device=DEV) if n_iter == 6 else ws
+        C_ref = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+        occ.occ_gemm(A, B, C_ref)
+        if kind == "own":
+            C = torch.full((n_iter, M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+            peers = inputs.reduce_chunks(3, M * N, seed=4, device=DEV)
+            comm = dict(bufs=peers, out=torch.full((M * N,), float("nan"), device=DEV), reduce_own=True)
+        else:
+            C = torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16)
+            if kind == "reduce":
+                chunks = inputs.reduce_chunks(4, 1 << 18, seed=1, device=DEV)
+                comm = dict(bufs=chunks, out=torch.full((1 << 18,), float("nan"), device=DEV))
+            else:
+                src = inputs.permute_payload(16, 1 << 14, seed=2, device=DEV)
+                perm = inputs.chunk_permutation(16, seed=3)
+                comm = dict(src=src, dst=torch.zeros_like(src), perm=perm, chunk_bytes=1 << 14)
+        torch.cuda.synchronize()                      # both streams follow the inputs
+        occ.occ_overlap_enqueue(A, B, C, workspace=ws, comm_stream=s1, err=err, n_iter=n_iter, **comm)
+        torch.cuda.synchronize()
+        assert int(err.item()) == 0
+        assert int(ws.abs().sum().item()) == 0        # every counter back at zero
+        if kind == "own":
+            for i in range(n_iter):
+                assert torch.equal(C[i].view(torch.int16), C_ref.view(torch.int16)), i
+            ref = oracle.chunk_sum_own_f32(C[-1].cpu(), peers.cpu().numpy())
+            assert np.array_equal(comm["out"].cpu().numpy().view(np.uint32), ref.view(np.uint32))
+        else:
+            assert torch.equal(C.view(torch.int16), C_ref.view(torch.int16))
+            if kind == "reduce":
+                ref = oracle.chunk_sum_f32(chunks.cpu().numpy())
+                assert np.array_equal(comm["out"].cpu().numpy().view(np.uint32), ref.view(np.uint32))
+            else:
+                want = oracle.permute_chunks(src.cpu().numpy(), perm.numpy(), 1 << 14)
+                assert np.array_equal(comm["dst"].cpu().numpy(), want)
+
+
+def test_overlap_enqueue_rejects_what_it_cannot_run():
+    A, B, C, chunks, out = reduce_setup()
+    s1 = torch.cuda.Stream()
+    cus = occ.occ_gemm_plan_query(512, 512, 512)["num_cus"]
+    ws = torch.zeros(occ.occ_overlap_workspace_bytes(4) // 4, dtype=torch.int32, device=DEV)
+    with pytest.raises(occ.OccError) as e:            # more than one comm workgroup per CU
+        occ.occ_overlap_enqueue(A, B, C, workspace=ws, comm_stream=s1, bufs=chunks, out=out, n_iter=4,
+                                comm_wgs=cus + 1)
+    assert e.value.status == occ.OCC_EINVAL
+    with pytest.raises(occ.OccError) as e:            # workspace too short for 64 iterations
+        occ.occ_overlap_enqueue(A, B, C, workspace=ws, comm_stream=s1, bufs=chunks, out=out, n_iter=64)
+    assert e.value.status == occ.OCC_EINVAL
+    torch.cuda.synchronize()
+    assert int(ws.abs().sum().item()) == 0            # nothing was launched
