@@ -206,7 +206,7 @@ static int fill_plan(const GemmCall &c, int variant, const DeviceInfo &di, occ_g
 // The launch plan without the occupancy figure: all a launch needs (the
 // occupancy query costs host time on every call, which launch-bound
 // schedules cannot spare).
-static int launch_plan(const GemmCall &c, occ_gemm_plan *plan) {
+int gemm_launch_plan(const GemmCall &c, occ_gemm_plan *plan) {
   const DeviceInfo *di = nullptr;
   int st = current_device_info(&di);
   if (st != OCC_OK) return st;
@@ -216,7 +216,7 @@ static int launch_plan(const GemmCall &c, occ_gemm_plan *plan) {
 }
 
 int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
-  int st = launch_plan(c, plan);
+  int st = gemm_launch_plan(c, plan);
   if (st != OCC_OK) return st;
   const Variant *v = find_variant(plan->kernel_id);
   int dyn = (int)(v->fn ? v->lds + c.lds_bytes : c.lds_bytes);
@@ -230,7 +230,7 @@ int gemm_plan(const GemmCall &c, occ_gemm_plan *plan) {
 
 int gemm_launch(const GemmCall &c, hipStream_t s) {
   occ_gemm_plan p;
-  int st = launch_plan(c, &p);
+  int st = gemm_launch_plan(c, &p);
   if (st != OCC_OK) return st;
   if (c.M == 0 || c.N == 0) return OCC_OK;
   const Variant *v = find_variant(p.kernel_id);

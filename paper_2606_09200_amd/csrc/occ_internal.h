@@ -39,6 +39,8 @@ struct GemmCall {
   bool b_kn = false;    // B stored K x N (occ_gemm: C = A B) or N x K (occ_gemm_bt: C = A B^T)
 };
 int gemm_plan(const GemmCall &c, occ_gemm_plan *plan);
+// the plan without the occupancy figure (wg_per_cu = 0): no runtime query
+int gemm_launch_plan(const GemmCall &c, occ_gemm_plan *plan);
 bool gemm_variant_is_kn(int id);  // a variant that takes B stored K x N
 int gemm_launch(const GemmCall &c, hipStream_t s);
 

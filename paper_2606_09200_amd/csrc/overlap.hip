@@ -272,18 +272,20 @@ int comm_grid(const occ_overlap_cfg &c, const Launcher &L) {
 // Per-iteration hooks of the counter dependency over `n` iterations with
 // counters tk[0..n) (GEMM workgroups done) and ack[0..n) (collective
 // workgroups past their wait), timeouts reported in *err.
+void counter_hook_pair(const Launcher &L, int i, uint32_t gemm_grid, uint32_t *tk, uint32_t *ack, uint32_t *err,
+                       KHooks *hg, KHooks *hc) {
+  hg->signal = tk + i;
+  hg->release = L.own ? 1u : 0u;
+  hc->wait = tk + i;
+  hc->ack = ack + i;
+  hc->err = err;
+  hc->wait_target = (L.g.M > 0 && L.g.N > 0) ? gemm_grid : 0u;
+  hc->acquire = L.own ? 1u : 0u;
+}
+
 void counter_hooks(const Launcher &L, int n, uint32_t gemm_grid, uint32_t *tk, uint32_t *ack, uint32_t *err,
                    std::vector<KHooks> *hg, std::vector<KHooks> *hc) {
-  const uint32_t target = (L.g.M > 0 && L.g.N > 0) ? gemm_grid : 0u;
-  for (int i = 0; i < n; ++i) {
-    (*hg)[i].signal = tk + i;
-    (*hg)[i].release = L.own ? 1u : 0u;
-    (*hc)[i].wait = tk + i;
-    (*hc)[i].ack = ack + i;
-    (*hc)[i].err = err;
-    (*hc)[i].wait_target = target;
-    (*hc)[i].acquire = L.own ? 1u : 0u;
-  }
+  for (int i = 0; i < n; ++i) counter_hook_pair(L, i, gemm_grid, tk, ack, err, &(*hg)[i], &(*hc)[i]);
 }
 
 int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res) {
@@ -591,14 +593,14 @@ int enqueue_impl(const occ_overlap_cfg *cfg, hipStream_t s1, uint32_t *tk, uint3
   make_launcher(c, &L);
   if (comm_grid(c, L) > di->num_cus) return OCC_EINVAL;
   occ_gemm_plan plan;
-  OCC_TRY(gemm_plan(L.g, &plan));
-  const int n = c.n_iter;
-  std::vector<KHooks> hg(n), hc(n);
-  counter_hooks(L, n, (uint32_t)plan.grid, tk, ack, err != nullptr ? err : err_sink, &hg, &hc);
+  OCC_TRY(gemm_launch_plan(L.g, &plan));
   hipStream_t s0 = static_cast<hipStream_t>(c.stream);
-  for (int i = 0; i < n; ++i) {
-    OCC_TRY(L.gemm(s0, hg[i], i));
-    OCC_TRY(L.comm(s1, hc[i], true, i));
+  // nothing here allocates: the hooks of each iteration live on the stack
+  for (int i = 0; i < c.n_iter; ++i) {
+    KHooks hg{}, hc{};
+    counter_hook_pair(L, i, (uint32_t)plan.grid, tk, ack, err != nullptr ? err : err_sink, &hg, &hc);
+    OCC_TRY(L.gemm(s0, hg, i));
+    OCC_TRY(L.comm(s1, hc, true, i));
   }
   return OCC_OK;
 }
