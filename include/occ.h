@@ -440,6 +440,21 @@ size_t occ_overlap_workspace_bytes(int n_iter);
 int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
                         uint32_t *err);
 
+/*
+ * occ_overlap_enqueue_noalloc -- occ_overlap_enqueue for callers that cannot
+ * allocate device memory (code under graph capture, tight serving loops,
+ * harnesses that forbid allocation): the counters live in a library-owned
+ * static device array sized for OCC_NOALLOC_MAX_ITER iterations (8448 bytes
+ * on every GPU the library runs on, held until the process ends), so no
+ * workspace is passed and nothing is allocated.  n_iter above
+ * OCC_NOALLOC_MAX_ITER is OCC_EINVAL.  All calls on one GPU share that
+ * array: calls that overlap on one GPU race (order each call's cfg->stream
+ * after the previous call's comm_stream).  The array starts zeroed and a
+ * complete schedule leaves it zeroed.  Otherwise as occ_overlap_enqueue.
+ */
+#define OCC_NOALLOC_MAX_ITER 1024
+int occ_overlap_enqueue_noalloc(const occ_overlap_cfg *cfg, void *comm_stream, uint32_t *err);
+
 /* Static string naming a status code. */
 const char *occ_strerror(int status);
 
@@ -447,7 +462,7 @@ const char *occ_strerror(int status);
    structure above gains fields, so a binding can refuse a library whose
    layout it does not know. */
 #define OCC_VERSION_MAJOR 2
-#define OCC_VERSION_MINOR 1
+#define OCC_VERSION_MINOR 2
 int occ_version(void);
 
 #ifdef __cplusplus

@@ -34,7 +34,8 @@ NK_VARIANTS = {
     25: "dl+pipe 128x256x32 4w 2st 2wg/cu", 34: "skinny M<=16, A in registers, B through LDS (K%1024==0, K<=8192)",
 }
 SKINNY_VARIANTS = (21, 33, 34)     # M <= 16 only
-ABI_VERSION = (2, 1)      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
+ABI_VERSION = (2, 2)
+NOALLOC_MAX_ITER = 1024   # OCC_NOALLOC_MAX_ITER      # OCC_VERSION_MAJOR, OCC_VERSION_MINOR of the structures below
 MIN_COMM_RATE_GBS = 10.0  # OCC_MIN_COMM_RATE_GBS
 WG_RECORD_WORDS = 12    # uint32 words per workgroup record in a wg_trace buffer
 
@@ -103,6 +104,7 @@ _SIGS = {
                          ctypes.POINTER(occ_overlap_result), ctypes.POINTER(ctypes.c_int)],
     "occ_overlap_workspace_bytes": [ctypes.c_int],
     "occ_overlap_enqueue": [ctypes.POINTER(occ_overlap_cfg), _P, _P, ctypes.c_size_t, _P],
+    "occ_overlap_enqueue_noalloc": [ctypes.POINTER(occ_overlap_cfg), _P, _P],
     "occ_strerror": [ctypes.c_int],
     "occ_version": [],
 }
@@ -448,3 +450,18 @@ def occ_overlap_enqueue(A, B, C, *, workspace, comm_stream, err=None, bufs=None,
     _check(lib().occ_overlap_enqueue(ctypes.byref(cfg), _stream(comm_stream), _ptr(workspace),
                                      workspace.numel() * workspace.element_size(), _ptr(err)),
            "occ_overlap_enqueue")
+
+
+def occ_overlap_enqueue_noalloc(A, B, C, *, comm_stream, err=None, bufs=None, out=None, src=None, dst=None,
+                                perm=None, chunk_bytes=0, lds_bytes=0, gemm_variant=0, gemm_grid=0,
+                                gemm_priority=0, comm_wgs=0, comm_priority=0, n_iter=10, comm_rate_gbs=0.0,
+                                b_layout="kn", reduce_own=False, stream=None):
+    """occ_overlap_enqueue with the counters in the library's own static
+    device array (at most NOALLOC_MAX_ITER iterations): allocates nothing."""
+    cfg, keep = _make_cfg(A, B, C, bufs, out, src, dst, perm, chunk_bytes, lds_bytes, gemm_variant,
+                          gemm_grid, gemm_priority, comm_wgs, comm_priority, n_iter, 1, 0, 0, None, None,
+                          comm_rate_gbs, b_layout, reduce_own, "counter", stream)
+    if err is not None and (not err.is_cuda or err.element_size() != 4 or err.numel() < 1):
+        raise ValueError("err must be a 32-bit GPU tensor")
+    _check(lib().occ_overlap_enqueue_noalloc(ctypes.byref(cfg), _stream(comm_stream), _ptr(err)),
+           "occ_overlap_enqueue_noalloc")

@@ -103,6 +103,7 @@ int run_overlap_impl(const occ_overlap_cfg *cfg, occ_overlap_result *res);
 size_t overlap_workspace_bytes(int n_iter);
 int overlap_enqueue_impl(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
                          uint32_t *err);
+int overlap_enqueue_noalloc_impl(const occ_overlap_cfg *cfg, void *comm_stream, uint32_t *err);
 int overlap_tune_impl(occ_overlap_cfg *cfg, int tune_reps, occ_overlap_result *res,
                       int *prefer_sequential);
 
@@ -227,6 +228,10 @@ size_t occ_overlap_workspace_bytes(int n_iter) { return occ::overlap_workspace_b
 int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
                         uint32_t *err) {
   return occ::overlap_enqueue_impl(cfg, comm_stream, workspace, workspace_bytes, err);
+}
+
+int occ_overlap_enqueue_noalloc(const occ_overlap_cfg *cfg, void *comm_stream, uint32_t *err) {
+  return occ::overlap_enqueue_noalloc_impl(cfg, comm_stream, err);
 }
 
 const char *occ_strerror(int status) {

@@ -611,6 +611,37 @@ size_t overlap_workspace_bytes(int n_iter) {
   return (words * sizeof(uint32_t) + 255) & ~(size_t)255;
 }
 
+// The counters of occ_overlap_enqueue_noalloc: a library-owned device array
+// (one copy per GPU, zero from load), for callers that cannot allocate.  In
+// host code `scratch` names a host-side stand-in; its device address on the
+// current GPU comes from hipGetSymbolAddress, once per device, and only that
+// address is passed to kernels.
+constexpr int kNoallocMaxIter = OCC_NOALLOC_MAX_ITER;
+static __device__ __align__(256) uint32_t scratch[2 * kNoallocMaxIter + 64];
+uint32_t *g_scratch[64];  // device address of `scratch`, per device
+
+int noalloc_scratch(uint32_t **out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return OCC_ENODEV;
+  if (g_scratch[dev] == nullptr) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return OCC_EHIP;
+    g_scratch[dev] = static_cast<uint32_t *>(p);
+  }
+  *out = g_scratch[dev];
+  return OCC_OK;
+}
+
+int overlap_enqueue_noalloc_impl(const occ_overlap_cfg *cfg, void *comm_stream, uint32_t *err) {
+  if (cfg == nullptr || cfg->n_iter < 1 || cfg->n_iter > kNoallocMaxIter) return OCC_EINVAL;
+  const DeviceInfo *di = nullptr;
+  OCC_TRY(current_device_info(&di));
+  uint32_t *w = nullptr;
+  OCC_TRY(noalloc_scratch(&w));
+  return enqueue_impl(cfg, static_cast<hipStream_t>(comm_stream), w, w + kNoallocMaxIter, kNoallocMaxIter, err,
+                      w + 2 * kNoallocMaxIter);
+}
+
 int overlap_enqueue_impl(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
                          uint32_t *err) {
   if (cfg == nullptr || workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 3u) != 0)

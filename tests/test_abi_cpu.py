@@ -58,9 +58,9 @@ def test_strerror_and_version(L):
     for code in range(0, -8, -1):
         assert binding.occ_strerror(code).startswith("OCC_")
     assert "unknown" in binding.occ_strerror(-99)
-    assert binding.occ_version() == binding.ABI_VERSION == (2, 1)
+    assert binding.occ_version() == binding.ABI_VERSION == (2, 2)
     hdr = open(HEADER).read()
-    assert "#define OCC_VERSION_MAJOR 2" in hdr and "#define OCC_VERSION_MINOR 1" in hdr
+    assert "#define OCC_VERSION_MAJOR 2" in hdr and "#define OCC_VERSION_MINOR 2" in hdr
 
 
 P = ctypes.c_void_p
@@ -279,3 +279,18 @@ def test_overlap_enqueue_argument_errors(L):
     expect_accepted(L, L.occ_overlap_enqueue, ctypes.byref(cfg), None, ws, 256, None)
     cfg.n_iter = 0
     assert L.occ_overlap_enqueue(ctypes.byref(cfg), None, ws, 256, None) == -1
+
+
+def test_overlap_enqueue_noalloc_argument_errors(L):
+    from paper_2606_09200_amd import binding as b
+    assert b.NOALLOC_MAX_ITER == 1024 and "#define OCC_NOALLOC_MAX_ITER 1024" in open(HEADER).read()
+    cfg = b.occ_overlap_cfg()
+    cfg.M = cfg.N = cfg.K = 8
+    cfg.A, cfg.B, cfg.C = 0x1000, 0x2000, 0x3000
+    arr = (ctypes.c_void_p * 2)(0x10000, 0x20000)
+    cfg.bufs = ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p))
+    cfg.nchunks, cfg.len, cfg.out = 2, 64, 0x30000
+    assert L.occ_overlap_enqueue_noalloc(None, None, None) == -1
+    for n in (0, -3, 1025):                                                       # beyond the array
+        cfg.n_iter = n
+        assert L.occ_overlap_enqueue_noalloc(ctypes.byref(cfg), None, None) == -1, n
