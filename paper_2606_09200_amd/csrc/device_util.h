@@ -66,12 +66,17 @@ __device__ __forceinline__ void dep_wait(const KHooks &t) {
   if (threadIdx.x == 0) {
     const uint64_t t0 = now_ticks();
     bool late = false;
+    // poll every ~128 cycles for the first 5 us (launch-bound schedules),
+    // then every ~2000 cycles: a long wait (its GEMM takes milliseconds)
+    // then puts little load on the memory system the GEMM is using
     while (__hip_atomic_load(t.wait, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < t.wait_target) {
-      if (now_ticks() - t0 > kDepWaitTicks) {
+      const uint64_t waited = now_ticks() - t0;
+      if (waited > kDepWaitTicks) {
         late = true;
         break;
       }
-      __builtin_amdgcn_s_sleep(2);
+      if (waited < 500) __builtin_amdgcn_s_sleep(2);
+      else __builtin_amdgcn_s_sleep(32);
     }
     if (late) __hip_atomic_store(t.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (t.acquire) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
