@@ -435,7 +435,9 @@ size_t occ_overlap_workspace_bytes(int n_iter);
  * must run the two streams' chains concurrently, as captured.
  * Errors: those of run_overlap, and OCC_EINVAL for a NULL, misaligned or
  * short workspace, a comm grid above one workgroup per CU, or a collective
- * with no work.
+ * with no work.  Every argument is checked before the first launch; only a
+ * runtime failure (OCC_EHIP) can stop the call part-way, and then counts of
+ * the launched GEMMs may remain in the workspace: zero it before reusing it.
  */
 int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *workspace, size_t workspace_bytes,
                         uint32_t *err);
@@ -450,7 +452,9 @@ int occ_overlap_enqueue(const occ_overlap_cfg *cfg, void *comm_stream, void *wor
  * OCC_NOALLOC_MAX_ITER is OCC_EINVAL.  All calls on one GPU share that
  * array: calls that overlap on one GPU race (order each call's cfg->stream
  * after the previous call's comm_stream).  The array starts zeroed and a
- * complete schedule leaves it zeroed.  Otherwise as occ_overlap_enqueue.
+ * complete schedule leaves it zeroed (after an OCC_EHIP part-way through a
+ * call it may not be: the library's array cannot then be reused safely in
+ * this process).  Otherwise as occ_overlap_enqueue.
  */
 #define OCC_NOALLOC_MAX_ITER 1024
 int occ_overlap_enqueue_noalloc(const occ_overlap_cfg *cfg, void *comm_stream, uint32_t *err);
