@@ -34,6 +34,9 @@ CONFIGS = ("tiny", "cb", "mb", "a2a", "sweep")
 # workgroup per four CUs); its record also carries the default comm grid.
 CONFIG_DEP = {"tiny": "counter"}
 CONFIG_COMM_WGS_PER_CU = {"tiny": 0.25}
+# Extra GEMM LDS pads a workload's record also reports, at both comm
+# priorities (the tiny pair's definition: pad {0, 64 KiB} x priority).
+CONFIG_EXTRA_PADS_KIB = {"tiny": (64,)}
 SWEEP_PADS_KIB = (0, 16, 32, 64, 96, 128)
 SWEEP_TILES = ((0, "default tile"), (37, "opt2 64x64x64"))
 
@@ -492,6 +495,27 @@ def main():
                     d[dd] = {"t_seq_ms": round(rd["t_seq_median_ms"], 4), "t_ovl_ms": round(rd["t_ovl_median_ms"], 4),
                              "reduction_pct": round(100.0 * (1.0 - rd["t_ovl_median_ms"] / rd["t_seq_median_ms"]), 3)}
                 rec["default_comm_grid"] = dict(d, comm_wgs=rd["comm_wgs"], note="medians")
+            pads = []
+            for pad_kib in CONFIG_EXTRA_PADS_KIB.get(name, ()):
+                pp = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K, pad_kib << 10)
+                row = {"pad_kib": pad_kib, "gemm_wg_per_cu": pp["wg_per_cu"] if pp["feasible"] else 0}
+                if pp["feasible"]:
+                    rp = {}
+                    for prio in (3, 0):
+                        rp[prio] = occ.run_overlap(A, B, C, reps=args.steps, warmup=args.warmup,
+                                                   flags=occ.OCC_RUN_SEQ | occ.OCC_RUN_OVL,
+                                                   **dict(kn, lds_bytes=pad_kib << 10, comm_priority=prio, dep=cdep),
+                                                   **comm)
+                    row.update({"t_seq_ms": round(rp[3]["t_seq_median_ms"], 4),
+                                "t_ovl_ms": round(rp[3]["t_ovl_median_ms"], 4),
+                                "t_ovl_normal_priority_ms": round(rp[0]["t_ovl_median_ms"], 4),
+                                "reduction_pct": round(100.0 * (1.0 - rp[3]["t_ovl_median_ms"] / rp[3]["t_seq_median_ms"]), 3),
+                                "reduction_pct_normal_priority": round(
+                                    100.0 * (1.0 - rp[0]["t_ovl_median_ms"] / rp[3]["t_seq_median_ms"]), 3),
+                                "note": "medians"})
+                pads.append(row)
+            if pads:
+                rec["extra_pads"] = pads
             rec["tuned"] = tuned(occ, wc, A, B, C, comm, args.steps)
             rec["roofline"] = roofline(wc, rc, "occ_gemm variant %d" % pc["kernel_id"], "kn")
             if not args.no_cpu_baseline:
