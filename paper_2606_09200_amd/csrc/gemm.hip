@@ -133,6 +133,7 @@ const Variant kVariants[] = {
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
+constexpr int kMaxDevices = 64;    // and by device
 
 bool is_skinny(const Variant *v) { return v->skinny != nullptr; }
 
@@ -237,27 +238,31 @@ int gemm_launch(const GemmCall &c, hipStream_t s) {
   const uint16_t *A = static_cast<const uint16_t *>(c.A);
   const uint16_t *B = static_cast<const uint16_t *>(c.B);
   uint16_t *C = static_cast<uint16_t *>(c.C);
+  // the dynamic-LDS limit is a per-device attribute of each kernel: set it
+  // once per device and variant
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return OCC_ENODEV;
   if (v->fn) {
     int dyn = v->lds + (int)c.lds_bytes;
-    static bool attr_set[kMaxVariantId + 1] = {};
-    if (!attr_set[v->id]) {
+    static bool attr_set[kMaxDevices][kMaxVariantId + 1] = {};
+    if (!attr_set[dev][v->id]) {
       if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->fn),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
                               p.max_lds_per_wg) != hipSuccess)
         return OCC_EHIP;
-      attr_set[v->id] = true;
+      attr_set[dev][v->id] = true;
     }
     int tiles_m = ceil_div(c.M, v->bm), tiles_n = ceil_div(c.N, v->bn);
     hipLaunchKernelGGL(v->fn, dim3(p.grid), dim3(v->threads), dyn, s, A, B, C, c.M, c.N, c.K,
                        tiles_m, tiles_n, c.priority, c.trace);
   } else {
-    static bool attr_set_skinny[kMaxVariantId + 1] = {};
-    if (!attr_set_skinny[v->id]) {
+    static bool attr_set_skinny[kMaxDevices][kMaxVariantId + 1] = {};
+    if (!attr_set_skinny[dev][v->id]) {
       if (hipFuncSetAttribute(reinterpret_cast<const void *>(v->skinny),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
                               p.max_lds_per_wg - v->lds) != hipSuccess)
         return OCC_EHIP;
-      attr_set_skinny[v->id] = true;
+      attr_set_skinny[dev][v->id] = true;
     }
     hipLaunchKernelGGL(v->skinny, dim3(p.grid), dim3(v->threads), (int)c.lds_bytes, s, A, B, C,
                        c.M, c.N, c.K, c.priority, c.trace);
