@@ -503,6 +503,41 @@ def test_overlap_enqueue_matches_plain_calls(kind):
                 assert np.array_equal(comm["dst"].cpu().numpy(), want)
 
 
+def test_overlap_enqueue_back_to_back_without_host_sync():
+    """A serving loop: five schedules on one workspace, each one's GEMM stream
+    ordered after the previous one's collectives by a stream event only, no
+    host synchronisation in between (so a collective's counter reset and the
+    next schedule's GEMM are ordered by the device alone).  Every output is
+    right, no wait runs out, and the workspace ends at zero."""
+    M, N, K = 520, 264, 136
+    A, Bt = inputs.gemm_operands(M, N, K, seed=5, device=DEV)
+    B = Bt.t().contiguous()
+    C_ref = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm(A, B, C_ref)
+    n_iter, rounds = 4, 5
+    chunks = [inputs.reduce_chunks(4, 1 << 18, seed=10 + r, device=DEV) for r in range(rounds)]
+    outs = [torch.full((1 << 18,), float("nan"), device=DEV) for _ in range(rounds)]
+    Cs = [torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16) for _ in range(rounds)]
+    ws = torch.zeros(occ.occ_overlap_workspace_bytes(n_iter) // 4, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s0 = torch.cuda.current_stream()
+    s1 = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        occ.occ_overlap_enqueue(A, B, Cs[r], workspace=ws, comm_stream=s1, err=err, n_iter=n_iter,
+                                bufs=chunks[r], out=outs[r])
+        done = torch.cuda.Event()
+        done.record(s1)
+        s0.wait_event(done)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    assert int(ws.abs().sum().item()) == 0
+    for r in range(rounds):
+        assert torch.equal(Cs[r].view(torch.int16), C_ref.view(torch.int16)), r
+        ref = oracle.chunk_sum_f32(chunks[r].cpu().numpy())
+        assert np.array_equal(outs[r].cpu().numpy().view(np.uint32), ref.view(np.uint32)), r
+
+
 def test_overlap_enqueue_rejects_what_it_cannot_run():
     A, B, C, chunks, out = reduce_setup()
     s1 = torch.cuda.Stream()

@@ -73,6 +73,36 @@ def test_enqueue_noalloc_matches_workspace_entry_point(kind):
             assert np.array_equal(comm["dst"].cpu().numpy(), want)
 
 
+def test_enqueue_noalloc_back_to_back_without_host_sync():
+    """Four schedules in a row on the library's array, each one's GEMM stream
+    ordered after the previous one's collectives by a stream event only (no
+    host synchronisation): every output is the oracle's and no wait runs
+    out, so each schedule left the array at zero for the next."""
+    M, N, K, n_iter = 264, 136, 200, 5
+    A, B, _, _, _ = _case(M, N, K, n_iter, "reduce", seed=7)
+    rounds = 4
+    Cs = [torch.full((M, N), float("nan"), device=DEV, dtype=torch.bfloat16) for _ in range(rounds)]
+    chunks = [inputs.reduce_chunks(3, 70001, seed=20 + r, device=DEV) for r in range(rounds)]
+    outs = [torch.full((70001,), float("nan"), device=DEV) for _ in range(rounds)]
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    s0 = torch.cuda.current_stream()
+    s1 = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for r in range(rounds):
+        occ.occ_overlap_enqueue_noalloc(A, B, Cs[r], comm_stream=s1, err=err, n_iter=n_iter, bufs=chunks[r],
+                                        out=outs[r])
+        done = torch.cuda.Event()
+        done.record(s1)
+        s0.wait_event(done)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.gemm_bf16(bf16_bits(A), bf16_bits(B), M, N, K, b_layout="kn")
+    for r in range(rounds):
+        assert_gemm_close(bf16_bits(Cs[r]), ref, 1.0, 1.0, K, "noalloc C, round %d" % r)
+        want = oracle.chunk_sum_f32(chunks[r].cpu().numpy())
+        assert np.array_equal(outs[r].cpu().numpy().view(np.uint32), want.view(np.uint32)), r
+
+
 def test_enqueue_noalloc_rejects_more_iterations_than_its_array():
     A, B, C, comm, _ = _case(264, 136, 200, 1, "reduce", seed=1)
     s1 = torch.cuda.Stream()
