@@ -304,6 +304,36 @@ def test_gemm_bt_direct_to_lds_k_limit():
     assert occ.occ_gemm_plan_query(4096, 4096, (1 << 22) + 8)["kernel_id"] == OPT2_KN
 
 
+def test_gemm_at_the_direct_to_lds_k_limit():
+    """K at the 256x256 tile's limit, 2^22: one operand tile spans 2^31 bytes
+    of 32-bit offsets.  Variant 32 (B K x N), variant 16 (B N x K) and the
+    automatic choice agree bit for bit, and sampled 4 x 4 blocks (corners
+    and the middle) match the oracle; K + 8 is refused by the 256-wide tiles."""
+    M = N = 256
+    K = 1 << 22
+    assert occ.occ_gemm_plan_query(M, N, K, 0, 32)["kernel_id"] == 32
+    with pytest.raises(occ.OccError) as e:
+        occ.occ_gemm_plan_query(M, N, K + 8, 0, 32)
+    assert e.value.status == occ.OCC_EINVAL
+    A, Bt = inputs.gemm_operands(M, N, K, seed=9, device=DEV)
+    B = Bt.t().contiguous()
+    C32 = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    C16 = torch.empty_like(C32)
+    Cauto = torch.empty_like(C32)
+    occ.occ_gemm_ex(A, B, C32, variant=32)
+    occ.occ_gemm_bt_ex(A, Bt, C16, variant=16)
+    occ.occ_gemm(A, B, Cauto)
+    torch.cuda.synchronize()
+    assert torch.equal(C32.view(torch.int16), C16.view(torch.int16))
+    assert torch.equal(C32.view(torch.int16), Cauto.view(torch.int16))
+    del Bt, C16, Cauto
+    Ah, Bh, Ch = bf16_bits(A), bf16_bits(B), bf16_bits(C32)
+    for r0 in (0, 126, 252):
+        for c0 in (0, 130, 252):
+            ref = oracle.gemm_bf16(Ah, Bh, M, N, K, b_layout="kn", rows=(r0, r0 + 4), cols=(c0, c0 + 4))
+            assert_gemm_close(Ch[r0:r0 + 4, c0:c0 + 4], ref, 1.0, 1.0, K, "K=2^22 block %d,%d" % (r0, c0))
+
+
 # ------------------------------------------------------------ skinny K x N
 @pytest.mark.parametrize("M", [1, 5, 16])
 @pytest.mark.parametrize("N,K", [(8, 8), (136, 40), (1000, 1032), (4104, 4096), (264, 8200), (128, 32)])
