@@ -334,6 +334,35 @@ def test_gemm_at_the_direct_to_lds_k_limit():
             assert_gemm_close(Ch[r0:r0 + 4, c0:c0 + 4], ref, 1.0, 1.0, K, "K=2^22 block %d,%d" % (r0, c0))
 
 
+def test_gemm_kn_at_its_n_limit():
+    """B stored K x N at the 256x256 tile's N limit, 2^24 columns: a k-step's
+    rows of B span 2^31 bytes of 32-bit offsets.  Variant 32 agrees bit for
+    bit with the N x K kernel on the transposed B in sampled column blocks
+    (the last columns included), and both match the oracle there; N + 8 is
+    refused by variant 32."""
+    M, N, K = 256, 1 << 24, 64
+    assert occ.occ_gemm_plan_query(M, N, K, 0, 32)["kernel_id"] == 32
+    with pytest.raises(occ.OccError) as e:
+        occ.occ_gemm_plan_query(M, N + 8, K, 0, 32)
+    assert e.value.status == occ.OCC_EINVAL
+    A, Bt = inputs.gemm_operands(M, N, K, seed=11, device=DEV)
+    B = Bt.t().contiguous()
+    C32 = torch.empty((M, N), device=DEV, dtype=torch.bfloat16)
+    occ.occ_gemm_ex(A, B, C32, variant=32)
+    C16 = torch.empty_like(C32)
+    occ.occ_gemm_bt_ex(A, Bt, C16, variant=16)
+    torch.cuda.synchronize()
+    del Bt
+    Ah, Bh = bf16_bits(A), bf16_bits(B)
+    for c0 in (0, 4104, N // 2 + 12, N - 4):
+        blk32 = C32[:, c0:c0 + 4].contiguous()
+        assert torch.equal(blk32.view(torch.int16), C16[:, c0:c0 + 4].contiguous().view(torch.int16)), c0
+        got = bf16_bits(blk32)
+        for r0 in (0, 252):
+            ref = oracle.gemm_bf16(Ah, Bh, M, N, K, b_layout="kn", rows=(r0, r0 + 4), cols=(c0, c0 + 4))
+            assert_gemm_close(got[r0:r0 + 4], ref, 1.0, 1.0, K, "N=2^24 block %d,%d" % (r0, c0))
+
+
 # ------------------------------------------------------------ skinny K x N
 @pytest.mark.parametrize("M", [1, 5, 16])
 @pytest.mark.parametrize("N,K", [(8, 8), (136, 40), (1000, 1032), (4104, 4096), (264, 8200), (128, 32)])
