@@ -141,6 +141,29 @@ def test_reduce_mixed_magnitudes_and_subnormals():
     assert np.array_equal(u32(gpu_reduce(c)), u32(oracle.chunk_sum_f32(c)))
 
 
+def test_reduce_infinities_overflow_and_nan():
+    # IEEE binary32 in the fixed order: overflow to +-inf, inf + finite, and
+    # NaN from inf + -inf or a NaN term (NaN payloads are the hardware's, so
+    # NaN positions are compared as a set and every other result bit-exact)
+    rng = np.random.default_rng(21)
+    L = 4099
+    c = rng.standard_normal((8, L)).astype(np.float32)
+    big = np.finfo(np.float32).max
+    c[0, ::23] = big
+    c[1, ::23] = big                        # overflow to +inf after the second term
+    c[6, ::29] = -big
+    c[2, ::13] = np.inf
+    c[4, ::17] = -np.inf                    # inf + -inf = NaN every 221st element
+    c[7, ::19] = np.nan
+    c[3, 5] = np.float32(2.0 ** 127)        # one term that stays finite
+    got = gpu_reduce(c)
+    ref = oracle.chunk_sum_f32(c)
+    nan_got, nan_ref = np.isnan(got), np.isnan(ref)
+    assert nan_ref.any() and np.isinf(ref).any()
+    assert np.array_equal(nan_got, nan_ref)
+    assert np.array_equal(u32(got[~nan_ref]), u32(ref[~nan_ref]))
+
+
 def test_reduce_all_ones_and_integers():
     assert np.all(gpu_reduce(np.ones((8, 5000), dtype=np.float32)) == 8.0)
     ci = np.random.default_rng(4).integers(-1024, 1025, size=(8, 5000))

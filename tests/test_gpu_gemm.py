@@ -91,6 +91,34 @@ def test_gemm_integer_operands_bit_exact(variant):
     assert np.array_equal(got, oracle.gemm_bf16(A, B, M, 152, 520, b_layout="kn"))
 
 
+def _bf16_isnan(bits):
+    return ((bits & 0x7F80) == 0x7F80) & ((bits & 0x007F) != 0)
+
+
+@pytest.mark.parametrize("layout,variant", [("kn", v) for v in [0] + KN_TILED + KN_SKINNY] +
+                         [("nk", v) for v in [0] + NK_TILED + NK_SKINNY + [LDSB]])
+def test_gemm_infinities_and_nan(layout, variant):
+    # IEEE specials in the operands: an infinite A entry makes its row +-inf
+    # (NaN where it meets a zero of B), a NaN in B makes its column NaN.
+    # Small-integer operands keep every finite output exact, so those are
+    # compared bit for bit; NaN outputs are compared as a set (their sign
+    # and payload are the hardware's).
+    small = variant in KN_SKINNY + NK_SKINNY + [LDSB]
+    M, N = (13, 264) if small else (300, 264)
+    K = 1024 if variant == LDSB else 200
+    A, B, Bt = int_operands(M, N, K, seed=31 + variant)
+    A[3, 7] = float("inf")
+    A[10, 20] = float("-inf")
+    B[5, 9] = float("nan")
+    Bt[9, 5] = float("nan")
+    got = run_gemm(A, B, variant=variant) if layout == "kn" else run_gemm_bt(A, Bt, variant=variant)
+    ref = oracle.gemm_bf16(A, B, M, N, K, b_layout="kn")
+    nan_ref = _bf16_isnan(ref)
+    assert nan_ref[:, 9].all() and nan_ref[3].any() and (ref[3] == 0x7F80).any() and (ref[10] == 0xFF80).any()
+    assert np.array_equal(_bf16_isnan(got), nan_ref)
+    assert np.array_equal(got[~nan_ref], ref[~nan_ref])
+
+
 def test_gemm_tiled_variants_agree_bitwise():
     # every K x N tile accumulates each output over k in the same order
     A, B, _ = operands(384, 320, 448, seed=11)
