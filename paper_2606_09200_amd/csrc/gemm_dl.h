@@ -243,6 +243,9 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
     }
     __syncthreads();  // every wave is done with the stages before the next tile's prologue
 
+    // C is written once and not read again by this kernel: non-temporal
+    // stores keep it from displacing operand lines in the caches (≈ 1 % on
+    // 8192^3)
     const int ncol = lane & 31;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
@@ -254,7 +257,7 @@ __global__ __launch_bounds__(T::NT, T::MINB) void gemm_dl_kernel(const uint16_t 
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int m = mb + 8 * (r >> 2) + (r & 3);
-            if (m < M) C[(size_t)m * N + n] = to_bf16(acc[i][j][r]);
+            if (m < M) __builtin_nontemporal_store(to_bf16(acc[i][j][r]), &C[(size_t)m * N + n]);
           }
         }
         // keep the accumulator reads of one block next to its stores (the
