@@ -354,18 +354,24 @@ def main():
                                    b_layout=args.b_layout)
 
     # the same GEMM through torch.mm (hipBLASLt) on the same operands: a
-    # same-run reference for the GEMM, context only
+    # same-run reference for the GEMM, context only.  Timed after half a
+    # second of back-to-back calls: an idle chip needs tens of milliseconds
+    # to reach its steady clock, and a short burst from idle reads 15-20 %
+    # slow.
     C2 = C[0] if C.dim() == 3 else C
     ref_mm = (lambda: torch.mm(A, B, out=C2)) if args.b_layout == "kn" else (lambda: torch.mm(A, B.t(), out=C2))
-    for _ in range(3):
-        ref_mm()
+    t_warm = time.time()
+    while time.time() - t_warm < 0.5:
+        for _ in range(20):
+            ref_mm()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(10):
+    for _ in range(20):
         ref_mm()
     e1.record()
     torch.cuda.synchronize()
-    hipblaslt_ms = e0.elapsed_time(e1) / 10
+    hipblaslt_ms = e0.elapsed_time(e1) / 20
 
     # a plain 1 GiB device-to-device copy: a measured HBM ceiling beside the spec peak
     src = torch.empty(1 << 28, dtype=torch.float32, device=dev)
