@@ -43,3 +43,23 @@ def test_sweep_table_renders_partial_rows():
     ncol = t[0].count("|")
     assert all(line.count("|") == ncol for line in t)
     assert "| 0.900 |" in t[2] and "| 9.7 |" in t[2]
+
+
+def test_power_sampler_reads_microwatts_per_phase(tmp_path):
+    # kernel_driver --sustain --power: samples a hwmon-style file (microwatts)
+    # per labelled phase and summarises median and maximum in watts
+    import time
+    sys.path.insert(0, ROOT)
+    from paper_2606_09200_amd import kernel_driver as kd
+    f = tmp_path / "power1_input"
+    f.write_text("250000000\n")
+    s = kd.PowerSampler(str(f))
+    s.start()
+    time.sleep(0.3)
+    s.phase = 0
+    f.write_text("1400000000\n")
+    time.sleep(0.3)
+    s.stop()
+    assert s.summary("idle").startswith("median 250 W, max 250 W")
+    assert "max 1400 W" in s.summary(0)
+    assert s.summary("never") == "no samples"
