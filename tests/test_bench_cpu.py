@@ -63,3 +63,11 @@ def test_power_sampler_reads_microwatts_per_phase(tmp_path):
     assert s.summary("idle").startswith("median 250 W, max 250 W")
     assert "max 1400 W" in s.summary(0)
     assert s.summary("never") == "no samples"
+
+
+def test_current_engine_clock_from_a_dpm_listing():
+    sys.path.insert(0, ROOT)
+    from paper_2606_09200_amd import kernel_driver as kd
+    assert kd.current_mhz("S: 102Mhz *\n0: 500Mhz\n1: 2400Mhz\n") == 102.0
+    assert kd.current_mhz("0: 500Mhz\n1: 2400Mhz *\n") == 2400.0
+    assert kd.current_mhz("0: 500Mhz\n1: 2400Mhz\n") is None
