@@ -37,6 +37,11 @@ CONFIG_COMM_WGS_PER_CU = {"tiny": 0.25}
 # Extra GEMM LDS pads a workload's record also reports, at both comm
 # priorities (the tiny pair's definition: pad {0, 64 KiB} x priority).
 CONFIG_EXTRA_PADS_KIB = {"tiny": (64,)}
+# GEMM tile of a workload's record where it is not the library's automatic
+# choice: the tiny pair runs the paper's opt2 tile (Table 1, 16 KiB, so the
+# 64 KiB pad leaves two workgroups per CU); its record also reports the
+# sequential schedule with the automatic choice.
+CONFIG_GEMM_VARIANT = {"tiny": 37}
 SWEEP_PADS_KIB = (0, 16, 32, 64, 96, 128)
 SWEEP_TILES = ((0, "default tile"), (37, "opt2 64x64x64"))
 
@@ -487,11 +492,21 @@ def main():
             A, B, C, comm = make_inputs(wc, dev, "kn")
             torch.cuda.synchronize()
             cdep = CONFIG_DEP.get(name, "event")
-            pc = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K)
+            cvar = CONFIG_GEMM_VARIANT.get(name, 0)
+            pc = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K, 0, cvar)
             cwgs = int(CONFIG_COMM_WGS_PER_CU.get(name, 0) * pc["num_cus"])
-            kn = dict(n_iter=wc.n_iter, comm_priority=3, b_layout="kn", comm_wgs=cwgs)
+            kn = dict(n_iter=wc.n_iter, comm_priority=3, b_layout="kn", comm_wgs=cwgs, gemm_variant=cvar)
             rc, rec = measure_workload(occ, wc, A, B, C, comm, kn, args.steps, args.warmup, cdep)
             rec = dict({"workload": describe(wc, "kn"), "gemm_variant": pc["kernel_id"]}, **rec)
+            if cvar:
+                # the sequential schedule with the library's automatic GEMM choice
+                pa = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K)
+                ra = occ.run_overlap(A, B, C, reps=args.steps, warmup=args.warmup,
+                                     flags=occ.OCC_RUN_SEQ | occ.OCC_RUN_ISO, **dict(kn, gemm_variant=0, dep=cdep),
+                                     **comm)
+                rec["automatic_gemm_choice"] = {"gemm_variant": pa["kernel_id"],
+                                                "t_seq_ms": round(ra["t_seq_median_ms"], 4),
+                                                "t_gemm_ms": round(ra["t_gemm_ms"], 5), "note": "medians"}
             if cwgs:
                 # the same pair with the library's default comm grid (one per CU)
                 d = {}
@@ -503,7 +518,7 @@ def main():
                 rec["default_comm_grid"] = dict(d, comm_wgs=rd["comm_wgs"], note="medians")
             pads = []
             for pad_kib in CONFIG_EXTRA_PADS_KIB.get(name, ()):
-                pp = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K, pad_kib << 10)
+                pp = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K, pad_kib << 10, cvar)
                 row = {"pad_kib": pad_kib, "gemm_wg_per_cu": pp["wg_per_cu"] if pp["feasible"] else 0}
                 if pp["feasible"]:
                     rp = {}

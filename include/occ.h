@@ -79,11 +79,14 @@ enum {
   OCC_GEMM_KN_SKINNY_4W_2ST = 33,       /* M <= 16: 128-column units over the whole K; default for M <= 16 */
   OCC_GEMM_KN_128x128x64_4W_3ST = 35,   /* default for mid-size shapes */
   OCC_GEMM_KN_OPT1_64x64x32 = 36,       /* Table 1 opt1, one stage */
-  OCC_GEMM_KN_OPT2_64x64x64 = 37,       /* Table 1 opt2, one stage; default for small shapes */
+  OCC_GEMM_KN_OPT2_64x64x64 = 37,       /* Table 1 opt2, one stage */
   OCC_GEMM_KN_128x256x32_4W_2ST = 38,   /* two resident workgroups per CU (48 KiB) */
+  OCC_GEMM_KN_64x64x64_4W_2ST = 39,     /* the opt2 tile with two stages; default for small shapes */
   /* B stored N x K (occ_gemm_bt) */
   OCC_GEMM_OPT1_64x64x32 = 6,           /* Table 1 opt1, register-staged, one stage */
-  OCC_GEMM_OPT2_64x64x64 = 7,           /* Table 1 opt2, register-staged, one stage; default for small shapes */
+  OCC_GEMM_OPT2_64x64x64 = 7,           /* Table 1 opt2, register-staged, one stage; default for a K
+                                           beyond the direct-to-LDS tiles' limit */
+  OCC_GEMM_DL_64x64x64_4W_2ST = 9,      /* direct-to-LDS, two stages; default for small shapes */
   OCC_GEMM_DL_128x128x64_4W_3ST = 14,   /* direct-to-LDS; default for mid-size shapes */
   OCC_GEMM_DLP_256x256x64_8W_2ST = 16,  /* direct-to-LDS; default for large shapes */
   OCC_GEMM_SKINNY_8W_U8 = 21,           /* M <= 16, any K: 8 waves, 8 k-blocks in flight per lane */

@@ -26,10 +26,10 @@ OCC_DEP_EVENT, OCC_DEP_COUNTER = 0, 1
 KN_VARIANTS = {
     32: "dl+pipe 256x256x64 8w 2st", 33: "skinny M<=16, 128-column units",
     35: "dl 128x128x64 4w 3st", 36: "opt1 64x64x32 1st", 37: "opt2 64x64x64 1st",
-    38: "dl+pipe 128x256x32 4w 2st 2wg/cu",
+    38: "dl+pipe 128x256x32 4w 2st 2wg/cu", 39: "dl 64x64x64 4w 2st",
 }
 NK_VARIANTS = {
-    6: "opt1 64x64x32 register-staged", 7: "opt2 64x64x64 register-staged",
+    6: "opt1 64x64x32 register-staged", 7: "opt2 64x64x64 register-staged", 9: "dl 64x64x64 4w 2st",
     14: "dl 128x128x64 4w 3st", 16: "dl+pipe 256x256x64 8w 2st", 21: "skinny M<=16, 8w, 8 k-blocks in flight",
     25: "dl+pipe 128x256x32 4w 2st 2wg/cu", 34: "skinny M<=16, A in registers, B through LDS (K%1024==0, K<=8192)",
 }

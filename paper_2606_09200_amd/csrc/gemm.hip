@@ -100,6 +100,9 @@ constexpr Variant make_skinny_ldsb_variant(int id, const char *name) {
 // B stored N x K (occ_gemm_bt)
 using T64x64_opt1 = Tile<64, 64, 32, 2, 2, 1>;   // Table 1 opt1: 64x64x32
 using T64x64_opt2 = Tile<64, 64, 64, 2, 2, 1>;   // Table 1 opt2: 64x64x64
+// the opt2 tile with two direct-to-LDS stages: the automatic choice for small
+// shapes (one k-step's DMA in flight while the previous one is used)
+using D64x64_4w_2s = Tile<64, 64, 64, 2, 2, 2>;
 using D128x128_4w_3s = Tile<128, 128, 64, 2, 2, 3>;
 using P256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true>;
 // two workgroups per CU: each has its own barriers, so one computes while the
@@ -112,12 +115,14 @@ using PKN256x256_8w_2s = Tile<256, 256, 64, 2, 4, 2, true, 1, true>;
 using KN128x128_4w_3s = Tile<128, 128, 64, 2, 2, 3, false, 1, true>;
 using KN64x64_opt1 = Tile<64, 64, 32, 2, 2, 1, false, 1, true>;   // Table 1 opt1, one stage
 using KN64x64_opt2 = Tile<64, 64, 64, 2, 2, 1, false, 1, true>;   // Table 1 opt2, one stage
+using KN64x64_4w_2s = Tile<64, 64, 64, 2, 2, 2, false, 1, true>;
 using PKN128x256k32_4w_2s = Tile<128, 256, 32, 1, 4, 2, true, 2, true>;
 
 const Variant kVariants[] = {
     // B stored N x K
     make_variant<T64x64_opt1>(6, "64x64x32 opt1, B N x K"),
     make_variant<T64x64_opt2>(7, "64x64x64 opt2, B N x K"),
+    make_dl_variant<D64x64_4w_2s>(9, "dl 64x64x64 4w 2st, B N x K"),
     make_dl_variant<D128x128_4w_3s>(14, "dl 128x128x64 4w 3st, B N x K"),
     make_dl_variant<P256x256_8w_2s>(16, "dl+pipe 256x256x64 8w 2st, B N x K"),
     make_skinny_variant<8, 8>(21, "skinny M<=16, 8 waves, unroll 8, B N x K"),
@@ -130,6 +135,7 @@ const Variant kVariants[] = {
     make_dl_variant<KN64x64_opt1>(36, "dl 64x64x32 opt1 1st, B K x N"),
     make_dl_variant<KN64x64_opt2>(37, "dl 64x64x64 opt2 1st, B K x N"),
     make_dl_variant<PKN128x256k32_4w_2s>(38, "dl+pipe 128x256x32 4w 2st 2wg/cu, B K x N"),
+    make_dl_variant<KN64x64_4w_2s>(39, "dl 64x64x64 4w 2st, B K x N"),
 };
 
 constexpr int kMaxVariantId = 63;  // launch-attribute caches are indexed by id
@@ -147,8 +153,9 @@ int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // The kernel for a shape: skinny for M <= 16, else the largest tile that
 // still gives at least one 256x256 tile per CU (or one 128x128 tile per two
-// CUs), else the paper's opt2 64x64x64 tile.  A K beyond what a direct-to-LDS
-// tile addresses with 32-bit offsets takes the 64x64 tile.
+// CUs), else the 64x64x64 tile with two stages.  A K beyond what a
+// direct-to-LDS tile addresses with 32-bit offsets takes the 64x64 tile, and
+// beyond that (B N x K) the register-staged opt2 tile.
 int auto_variant(int M, int N, int K, int num_cus, bool b_kn) {
   if (M <= 16) {
     if (b_kn) return 33;
@@ -157,12 +164,16 @@ int auto_variant(int M, int N, int K, int num_cus, bool b_kn) {
     if (K >= 1024 && K % 1024 == 0 && K <= 8192) return 34;
     return 21;
   }
-  const int large = b_kn ? 32 : 16, mid = b_kn ? 35 : 14, small = b_kn ? 37 : 7;
+  const int large = b_kn ? 32 : 16, mid = b_kn ? 35 : 14, small = b_kn ? 39 : 9;
   long long big = (long long)ceil_div(M, 256) * ceil_div(N, 256);
   long long mids = (long long)ceil_div(M, 128) * ceil_div(N, 128);
   int v = big >= num_cus ? large : (mids >= num_cus / 2 ? mid : small);
   const Variant *pv = find_variant(v);
-  if (pv->kmax > 0 && K > pv->kmax) v = small;
+  if (pv->kmax > 0 && K > pv->kmax) {
+    v = small;
+    pv = find_variant(v);
+    if (pv->kmax > 0 && K > pv->kmax && !b_kn) v = 7;
+  }
   return v;
 }
 

@@ -16,9 +16,9 @@ from gpu_common import DEV, assert_gemm_close, bf16_bits, sample_tiles
 
 pytestmark = pytest.mark.gpu
 
-KN_TILED = [32, 35, 36, 37, 38]           # occ_gemm_ex, M > 16
+KN_TILED = [32, 35, 36, 37, 38, 39]       # occ_gemm_ex, M > 16
 KN_SKINNY = [33]                          # occ_gemm_ex, M <= 16
-NK_TILED = [6, 7, 14, 16, 25]             # occ_gemm_bt_ex, M > 16
+NK_TILED = [6, 7, 9, 14, 16, 25]          # occ_gemm_bt_ex, M > 16
 NK_SKINNY = [21]                          # occ_gemm_bt_ex, M <= 16, any K
 LDSB = 34                                 # occ_gemm_bt_ex, M <= 16, K % 1024 == 0, K <= 8192
 OPT1_KN, OPT2_KN = 36, 37                 # the paper's Table 1 tiles, B K x N
@@ -127,7 +127,7 @@ def test_gemm_tiled_variants_agree_bitwise():
         assert np.array_equal(run_gemm(A, B, variant=v), base), v
 
 
-@pytest.mark.parametrize("variant", [0, 32, 35, 36, 37, 38, 33])
+@pytest.mark.parametrize("variant", [0, 32, 35, 36, 37, 38, 39, 33])
 def test_gemm_pad_and_grid_cap_do_not_change_result(variant):
     M = 16 if variant in KN_SKINNY else 520
     A, B, _ = operands(M, 384, 256, seed=5)
@@ -192,16 +192,16 @@ def test_gemm_info_matches_plan():
 
 
 def test_auto_choice_by_shape():
-    # large: 256x256; mid: 128x128 three stages; small: the paper's opt2
-    # tile; M <= 16: the skinny kernel
+    # large: 256x256; mid: 128x128 three stages; small: the opt2 tile with
+    # two stages; M <= 16: the skinny kernel
     assert occ.occ_gemm_plan_query(8192, 8192, 8192)["kernel_id"] == 32
     assert occ.occ_gemm_plan_query(2048, 2048, 4096)["kernel_id"] == 35
-    assert occ.occ_gemm_plan_query(512, 512, 512)["kernel_id"] == 37
+    assert occ.occ_gemm_plan_query(512, 512, 512)["kernel_id"] == 39
     assert occ.occ_gemm_plan_query(16, 28672, 8192)["kernel_id"] == 33
     assert occ.occ_gemm_plan_query(17, 28672, 8192)["kernel_id"] == 35    # 224 128x128 tiles
     assert occ.occ_gemm_bt_plan_query(8192, 8192, 8192)["kernel_id"] == 16
     assert occ.occ_gemm_bt_plan_query(2048, 2048, 4096)["kernel_id"] == 14
-    assert occ.occ_gemm_bt_plan_query(512, 512, 512)["kernel_id"] == 7
+    assert occ.occ_gemm_bt_plan_query(512, 512, 512)["kernel_id"] == 9
 
 
 def test_paper_tiles_lds_footprint():
@@ -272,7 +272,7 @@ def test_gemm_bt_tiled_variants_agree_bitwise_and_match_kn():
     assert np.array_equal(run_gemm(A, B), base)
 
 
-@pytest.mark.parametrize("variant", [0, 7, 16, 21])
+@pytest.mark.parametrize("variant", [0, 7, 9, 16, 21])
 def test_gemm_bt_pad_and_grid_cap_do_not_change_result(variant):
     M = 16 if variant in NK_SKINNY else 520
     A, _, Bt = operands(M, 384, 256, seed=5)
@@ -322,14 +322,16 @@ def test_gemm_bt_skinny_k_rules_and_choice():
 
 def test_gemm_bt_direct_to_lds_k_limit():
     # 32-bit pass offsets: K above the tile's limit is refused by that
-    # variant, and the automatic choice for such K is the 64x64 tile
+    # variant, and the automatic choice for such K is the 64x64 tile (for B
+    # N x K beyond that tile's own limit, the register-staged opt2 tile)
     big = (1 << 25) + 8
     with pytest.raises(occ.OccError) as e:
         occ.occ_gemm_bt_plan_query(4096, 4096, big, 0, 16)
     assert e.value.status == occ.OCC_EINVAL
     assert occ.occ_gemm_bt_plan_query(4096, 4096, big)["kernel_id"] == 7
     assert occ.occ_gemm_bt_plan_query(4096, 4096, 1 << 20)["kernel_id"] == 16
-    assert occ.occ_gemm_plan_query(4096, 4096, (1 << 22) + 8)["kernel_id"] == OPT2_KN
+    assert occ.occ_gemm_plan_query(4096, 4096, (1 << 22) + 8)["kernel_id"] == 39
+    assert occ.occ_gemm_bt_plan_query(4096, 4096, (1 << 22) + 8)["kernel_id"] == 9
 
 
 def test_gemm_at_the_direct_to_lds_k_limit():
