@@ -41,7 +41,7 @@ CONFIG_EXTRA_PADS_KIB = {"tiny": (64,)}
 # choice: the tiny pair runs the paper's opt2 tile (Table 1, 16 KiB, so the
 # 64 KiB pad leaves two workgroups per CU); its record also reports the
 # sequential schedule with the automatic choice.
-CONFIG_GEMM_VARIANT = {"tiny": 37}
+CONFIG_GEMM_VARIANT = {"tiny": {"kn": 37, "nk": 7}}
 SWEEP_PADS_KIB = (0, 16, 32, 64, 96, 128)
 SWEEP_TILES = ((0, "default tile"), (37, "opt2 64x64x64"))
 
@@ -332,8 +332,12 @@ def main():
     A, B, C, comm = make_inputs(w, dev, args.b_layout)
     torch.cuda.synchronize()
     dep = args.dep or CONFIG_DEP.get(w.name, "event")
-    knobs = dict(lds_bytes=args.pad_kib << 10, gemm_variant=args.variant, gemm_grid=args.gemm_grid,
-                 comm_wgs=args.comm_wgs, comm_priority=args.priority, n_iter=w.n_iter,
+    # the workload's own knobs where the command line leaves them at 0
+    variant = args.variant or CONFIG_GEMM_VARIANT.get(w.name, {}).get(args.b_layout, 0)
+    num_cus = occ.occ_gemm_plan_query(w.M, w.N, w.K, 0, variant, b_layout=args.b_layout)["num_cus"]
+    comm_wgs = args.comm_wgs or int(CONFIG_COMM_WGS_PER_CU.get(w.name, 0) * num_cus)
+    knobs = dict(lds_bytes=args.pad_kib << 10, gemm_variant=variant, gemm_grid=args.gemm_grid,
+                 comm_wgs=comm_wgs, comm_priority=args.priority, n_iter=w.n_iter,
                  comm_rate_gbs=args.comm_rate_gbs, b_layout=args.b_layout, dep=dep)
     gemm_name = "occ_gemm" if args.b_layout == "kn" else "occ_gemm_bt"
 
@@ -355,7 +359,7 @@ def main():
               "t_ovl_std_ms", "time_ratio", "t_gemm_ms", "t_comm_ms", "ideal_ovl_ms", "gemm_tflops",
               "gemm_mfma_frac", "gemm_hbm_frac", "comm_gbs", "comm_hbm_frac"):
         rec.pop(k, None)
-    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, args.variant, args.gemm_grid,
+    plan = occ.occ_gemm_plan_query(w.M, w.N, w.K, args.pad_kib << 10, variant, args.gemm_grid,
                                    b_layout=args.b_layout)
 
     # the same GEMM through torch.mm (hipBLASLt) on the same operands: a
@@ -492,7 +496,7 @@ def main():
             A, B, C, comm = make_inputs(wc, dev, "kn")
             torch.cuda.synchronize()
             cdep = CONFIG_DEP.get(name, "event")
-            cvar = CONFIG_GEMM_VARIANT.get(name, 0)
+            cvar = CONFIG_GEMM_VARIANT.get(name, {}).get("kn", 0)
             pc = occ.occ_gemm_plan_query(wc.M, wc.N, wc.K, 0, cvar)
             cwgs = int(CONFIG_COMM_WGS_PER_CU.get(name, 0) * pc["num_cus"])
             kn = dict(n_iter=wc.n_iter, comm_priority=3, b_layout="kn", comm_wgs=cwgs, gemm_variant=cvar)
